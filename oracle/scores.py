@@ -1,0 +1,36 @@
+"""Per-position prediction statistics (Section 2.1, Eq. 2 and Eq. threshold_pd; Section 2.2).
+
+For a logit row l over the vocabulary V:
+  P(x_i = v) = softmax(l)_v                                   (Eq. 2)
+  x_hat_i = argmax_v P, c_i = max_v P                          (top-1 token, confidence)
+  second-ranked token and its probability                      (the top-1/top-2 gap of Section 2.2)
+Ties go to the lowest token id (greedy decoding, Section 4 setup; the paper
+does not specify a tie rule). The [MASK] id is an ordinary member of V and is
+not suppressed.
+"""
+import numpy as np
+
+SENTINEL_ID = -1      # top1/top2 of rows that are not scored
+SENTINEL_CONF = -1.0  # conf/p2 of rows that are not scored
+
+
+def row_stats(logits: np.ndarray):
+    """Statistics of each row of ``logits`` [R, V] (float64).
+
+    Returns (top1 [R] int64, top2 [R] int64, conf [R], p2 [R], lse [R]) where
+    conf = P(top1), p2 = P(top2) and lse = log sum_v exp(l_v).
+    Computed from the materialised softmax and a stable sort on (-l, id).
+    """
+    l = np.asarray(logits, dtype=np.float64)
+    R, V = l.shape
+    order = np.argsort(-l, axis=1, kind="stable")      # equal values keep ascending id order
+    top1 = order[:, 0]
+    top2 = order[:, 1]
+    m = l[np.arange(R), top1]
+    e = np.exp(l - m[:, None])
+    z = e.sum(axis=1)
+    P = e / z[:, None]
+    conf = P[np.arange(R), top1]
+    p2 = P[np.arange(R), top2]
+    lse = m + np.log(z)
+    return top1, top2, conf, p2, lse

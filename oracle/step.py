@@ -1,0 +1,62 @@
+"""One denoising iteration's forward + statistics (Algorithm 1, Forward; Section 2.1).
+
+``step`` returns, for every sequence and position, the prediction statistics of
+the scored rows (``select.scored_mask``) and sentinels elsewhere:
+top1/top2 = -1, conf/p2 = -1, lse = 0.
+"""
+import numpy as np
+
+from .forward import forward, lm_logits
+from .scores import SENTINEL_CONF, SENTINEL_ID, row_stats
+from .select import scored_mask
+
+
+def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_boundary=True,
+         rope=True, return_logits_rows=None):
+    """Statistics dict with arrays [B, S]: top1, top2, conf, p2, lse.
+
+    kv: optional callable (b, layer) -> (Kc [Hkv,P,dh], Vc [Hkv,dh,P]) with prefix length ``kv_prefix``
+        given as attribute ``kv.prefix``; tokens are then at absolute positions prefix + i.
+    return_logits_rows: optional list of flat row indices b*S+i whose float64 logits are also returned
+        (key "logits", [len, V]); they need not be scored rows.
+    """
+    tokens = np.asarray(tokens)
+    B, S = tokens.shape
+    sc = scored_mask(tokens, p, gen_end, geom.mask_id, score_all)
+    out = {
+        "top1": np.full((B, S), SENTINEL_ID, np.int64),
+        "top2": np.full((B, S), SENTINEL_ID, np.int64),
+        "conf": np.full((B, S), SENTINEL_CONF),
+        "p2": np.full((B, S), SENTINEL_CONF),
+        "lse": np.zeros((B, S)),
+    }
+    want = {} if return_logits_rows is None else {int(r): n for n, r in enumerate(return_logits_rows)}
+    logits_out = None if return_logits_rows is None else np.empty((len(want), geom.vocab))
+    prefix = 0 if kv is None else kv.prefix
+    pos = prefix + np.arange(S)
+    for b in range(B):
+        extra = [i for i in range(S) if (b * S + i) in want]
+        rows = np.nonzero(sc[b])[0]
+        if len(rows) == 0 and not extra:
+            continue
+        kvb = None if kv is None else (lambda l, b=b: kv(b, l))
+        hf = forward(geom, weights, tokens[b], pos, kv=kvb, bf16_boundary=bf16_boundary, rope=rope)
+        if len(rows):
+            t1, t2, c, p2, lse = row_stats(lm_logits(weights, hf[rows]))
+            out["top1"][b, rows] = t1
+            out["top2"][b, rows] = t2
+            out["conf"][b, rows] = c
+            out["p2"][b, rows] = p2
+            out["lse"][b, rows] = lse
+        if extra:
+            lg = lm_logits(weights, hf[extra])
+            for n, i in enumerate(extra):
+                logits_out[want[b * S + i]] = lg[n]
+    if logits_out is not None:
+        out["logits"] = logits_out
+    return out
+
+
+def step_from_weights(workload, weights, tokens, p, kv=None, score_all=False, **kw):
+    """``step`` with geometry and generation end taken from a ``synth.Workload``."""
+    return step(workload.geom, weights, tokens, p, workload.gen_end, kv=kv, score_all=score_all, **kw)

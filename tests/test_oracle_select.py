@@ -1,0 +1,148 @@
+"""Pins for the oracle's statistics and selection rules (CPU)."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+from oracle.loop import noncontiguous_commit_set
+from oracle.select import compute_k, scored_mask, select_contiguous
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "select_cases.json")
+
+
+# ---------------------------------------------------------------- statistics (Section 2.1 / 2.2)
+
+def test_row_stats_against_scipy_and_bruteforce():
+    rng = np.random.default_rng(0)
+    l = rng.standard_normal((50, 300)) * 4
+    t1, t2, c, p2, lse = oracle.row_stats(l)
+    P = scipy.special.softmax(l, axis=1)
+    for r in range(50):                                 # brute-force scan
+        best = max(range(300), key=lambda v: (l[r, v], -v))
+        second = max((v for v in range(300) if v != best), key=lambda v: (l[r, v], -v))
+        assert (t1[r], t2[r]) == (best, second)
+        assert c[r] == pytest.approx(P[r].max(), rel=1e-12)
+        assert p2[r] == pytest.approx(P[r, second], rel=1e-12)
+    np.testing.assert_allclose(lse, scipy.special.logsumexp(l, axis=1), rtol=1e-13)
+
+
+def test_row_stats_special_cases():
+    V = 1000
+    t1, t2, c, p2, lse = oracle.row_stats(np.zeros((1, V)))       # uniform: conf = 1/V, ids 0 and 1
+    assert (t1[0], t2[0]) == (0, 1) and c[0] == pytest.approx(1 / V) and p2[0] == pytest.approx(1 / V)
+    assert lse[0] == pytest.approx(np.log(V))
+    l = np.zeros((1, V)); l[0, 17] = l[0, 400] = 5.0             # tie: lower id wins, equal probabilities
+    t1, t2, c, p2, _ = oracle.row_stats(l)
+    assert (t1[0], t2[0]) == (17, 400) and c[0] == p2[0]
+    l = np.zeros((1, V)); l[0, 999] = 1000.0                      # one-hot limit
+    t1, t2, c, p2, _ = oracle.row_stats(l)
+    assert t1[0] == 999 and t2[0] == 0 and c[0] == 1.0 and p2[0] < 1e-300
+
+
+def test_row_stats_invariants():
+    rng = np.random.default_rng(1)
+    V = 4096
+    l = rng.standard_normal((200, V)) * rng.uniform(0.1, 20, (200, 1))
+    t1, t2, c, p2, _ = oracle.row_stats(l)
+    assert (t1 != t2).all()
+    assert (c >= 1 / V - 1e-15).all() and (c <= 1).all()
+    assert (p2 <= c).all() and (p2 <= 1 - c + 1e-15).all()
+
+
+# ---------------------------------------------------------------- DCV (Section 3.2, Eq. compute_k)
+
+def test_golden_k_cases():
+    cases = json.load(open(GOLDEN))["k_cases"]
+    for case in cases:
+        assert compute_k(np.array(case["conf"]), case["tau"]) == case["K"], case["why"]
+
+
+@pytest.mark.parametrize("L", range(1, 13))
+def test_compute_k_exhaustive(L):
+    """K equals the index of the first failing entry (or L), for every pass/fail pattern of length L."""
+    tau = 0.7
+    for bits in itertools.product((0, 1), repeat=L):
+        conf = np.where(np.array(bits) == 1, 0.9, 0.3)
+        s = "".join(map(str, bits)) + "0"
+        assert compute_k(conf, tau) == s.index("0")
+
+
+def test_compute_k_thresholds_at_extremes():
+    rng = np.random.default_rng(2)
+    conf = rng.uniform(1e-6, 1, 64)
+    assert compute_k(conf, 0.0) == 64          # tau = 0: every window entry is accepted
+    assert compute_k(conf, 1.0) == 0           # tau >= 1: nothing is accepted (K_eff = 1)
+
+
+# ---------------------------------------------------------------- commit / drafts / remask
+
+@pytest.mark.parametrize("case", json.load(open(GOLDEN))["select_cases"], ids=lambda c: c["name"])
+def test_golden_select_cases(case):
+    tok = np.array([case["tokens"]])
+    x, p, kr, ke = select_contiguous(tok, np.array([case["p"]]), case["gen_end"], case["L"],
+                                     case["tau_commit"], case["tau_draft"], case["mask_id"],
+                                     np.array([case["top1"]]), np.array([case["conf"]]))
+    assert x[0].tolist() == case["expect_tokens"]
+    assert (p[0], kr[0], ke[0]) == (case["expect_p"], case["expect_K_raw"], case["expect_K_eff"])
+
+
+def _random_state(rng, B=6, S=80, mask=999):
+    tok = rng.integers(0, 900, (B, S))
+    p = rng.integers(5, S, B)
+    for b in range(B):
+        tok[b, p[b]:] = np.where(rng.random(S - p[b]) < 0.7, mask, tok[b, p[b]:])
+    return tok, p
+
+
+def test_select_rules_per_position():
+    """Each output position obeys exactly one of: prompt/committed (unchanged), commit, draft, remask."""
+    rng = np.random.default_rng(3)
+    mask, S, L, end = 999, 80, 12, 80
+    for trial in range(200):
+        tok, p = _random_state(rng, S=S, mask=mask)
+        sc = scored_mask(tok, p, end, mask)
+        conf = np.where(sc, rng.uniform(0, 1, tok.shape), -1.0)
+        top1 = np.where(sc, rng.integers(0, 900, tok.shape), -1)
+        tc, td = rng.uniform(0.2, 0.9), rng.uniform(0.8, 1.0)
+        x, pn, kr, ke = select_contiguous(tok, p, end, L, tc, td, mask, top1, conf)
+        for b in range(tok.shape[0]):
+            pb = p[b]
+            Le = min(L, end - pb)
+            first_fail = next((j for j in range(Le) if not conf[b, pb + j] > tc), Le)
+            assert kr[b] == first_fail and ke[b] == max(first_fail, 1) and pn[b] == pb + ke[b]
+            np.testing.assert_array_equal(x[b, :pb], tok[b, :pb])                       # history immutable
+            np.testing.assert_array_equal(x[b, pb:pn[b]], top1[b, pb:pn[b]])             # commit
+            np.testing.assert_array_equal(x[b, pn[b]:min(pn[b] + L, end)], mask)         # remask
+            for j in range(min(pn[b] + L, end), end):
+                if j < pb + L:                                                           # old window
+                    assert x[b, j] == tok[b, j]
+                elif tok[b, j] == mask and conf[b, j] > td:
+                    assert x[b, j] == top1[b, j]                                         # draft update
+                else:
+                    assert x[b, j] == tok[b, j]
+
+
+def test_no_progress_guard_flag_and_score_all():
+    tok = np.array([[1, 2, 9, 9, 9, 50, 9, 9]])
+    top1 = np.array([[-1, -1, 30, 31, 32, 33, 34, 35]])
+    conf = np.array([[-1, -1, 0.5, 0.99, 0.99, 0.995, 0.2, 0.99]])
+    x, p, kr, ke = select_contiguous(tok, np.array([2]), 8, 3, 0.7, 0.98, 9, top1, conf,
+                                     no_progress_guard=True)
+    assert (kr[0], ke[0], p[0]) == (0, 0, 2)
+    assert x[0].tolist() == [1, 2, 9, 9, 9, 50, 9, 35]            # nothing committed; drafts still update
+    x, p, kr, ke = select_contiguous(tok, np.array([2]), 8, 3, 0.7, 0.98, 9, top1, conf, score_all=True)
+    assert x[0].tolist() == [1, 2, 30, 9, 9, 9, 9, 35]             # window [3,6) re-masks position 5's redraft
+
+
+def test_contiguous_commits_subset_of_threshold_commits():
+    """For the same confidences, DCV's accepted window is a subset of Eq. threshold_pd's set."""
+    rng = np.random.default_rng(4)
+    for _ in range(500):
+        conf = rng.uniform(0, 1, 40)
+        tau = rng.uniform(0, 1)
+        K = compute_k(conf[10:26], tau)
+        assert set(range(10, 10 + K)) <= noncontiguous_commit_set(conf, 10, 26, tau)
