@@ -1,0 +1,167 @@
+/*
+ * dcl.h — C ABI of the MI355X (gfx950) DC-Leap denoising-iteration library (libdcl.so).
+ *
+ * One denoising iteration of a masked-diffusion LM under DC-Leap ("Draft-guided
+ * Contiguous Leaping", Algorithm 1 in Appendix A of the paper) is
+ *   (ii)  Forward(p_theta, x): a bidirectional transformer over every position, then the
+ *         per-position softmax over the vocabulary at the masked positions (Section 2.1, Eq. 2),
+ *         reduced to the top-1 token, its probability c_i (Eq. threshold_pd) and the runner-up
+ *         (the top-1/top-2 gap of Section 2.2)            -> dcl_denoise_step
+ *   (iii) the contiguous window length K (Section 3.2, Eq. compute_k),
+ *   (iv)  commit x[p, p+K), update drafts (Section 3.3, Eq. draft_update), advance p, and
+ *   (i)   re-mask the next window (Eq. remasking)          -> dcl_select_contiguous
+ *
+ * Conventions for every call:
+ *  - Pointers are DEVICE pointers unless a comment says "host".
+ *  - Every GPU call is asynchronous on `stream` (0 = the null stream). Argument checks are
+ *    synchronous, happen on the host before anything is launched, and never touch device memory.
+ *  - The caller owns every buffer (weights, tokens, p, statistics, KV cache, workspace). The
+ *    library allocates only the host-side model handle (and, inside dcl_load_weights only, a
+ *    temporary device staging buffer that it frees before returning). dcl_denoise_step and
+ *    dcl_select_contiguous never allocate.
+ *  - bfloat16 tensors are passed as raw 16-bit patterns (round-to-nearest-even bfloat16).
+ *  - Token ids are int32. Positions inside `tokens` are half-open ranges [a, b).
+ *  - A failed check returns a non-zero dcl_status and leaves a message for dcl_last_error();
+ *    no C++ exception crosses this interface. A device-side fault surfaces at the caller's next
+ *    synchronisation of `stream`.
+ *  - One model handle may be used from one stream at a time; concurrent steps need their own
+ *    workspaces.
+ */
+#ifndef DCL_H_
+#define DCL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DCL_OK = 0,
+  DCL_E_ARG = 1,          /* null pointer, size or range outside the documented domain */
+  DCL_E_UNSUPPORTED = 2,  /* geometry this build has no kernels for */
+  DCL_E_WORKSPACE = 3,    /* workspace or weight buffer smaller than required */
+  DCL_E_HIP = 4,          /* a HIP runtime call or kernel launch failed */
+  DCL_E_STATE = 5         /* object used in the wrong state (e.g. step before weights load) */
+} dcl_status;
+
+/* Model geometry: a pre-norm bidirectional transformer with RMSNorm, rotate-half RoPE, SwiGLU
+ * (the LLaDA / Dream base models of Section 4 setup). Host struct. Supported: head_dim 64 or
+ * 128; n_heads % n_kv_heads == 0; d_model, d_ffn multiples of 16; vocab >= 2;
+ * 0 <= mask_id < vocab; rms_eps > 0; rope_base > 1; 1 <= max_positions <= 65536. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab, mask_id;
+  float rms_eps;          /* RMSNorm epsilon */
+  float rope_base;        /* RoPE theta base */
+  int32_t qkv_bias;       /* 1: q/k/v projections carry a bias (Dream / Qwen2.5 geometry) */
+  int32_t rope_enabled;   /* 1 normally; 0 turns RoPE off (test support: permutation checks) */
+  int32_t max_positions;  /* largest absolute position + 1 that a step may use */
+} dcl_config;
+
+typedef struct dcl_model_s* dcl_model_t;
+
+/* Per-position prediction statistics, each array [B, S] (row b*S + i), device memory.
+ * Scored rows: top1 = argmax_v P(x_i = v), top2 = best other id (ties to the lowest id),
+ * conf = P(top1) (the confidence c_i), p2 = P(top2), lse = log sum_v exp(logit_v).
+ * Rows that are not scored: top1 = top2 = -1, conf = p2 = -1, lse = 0. */
+typedef struct {
+  int32_t* top1;
+  int32_t* top2;
+  float* conf;
+  float* p2;
+  float* lse;
+} dcl_row_stats;
+
+/* Cached prefix for the KV-cache step (dLLM-Cache combination, Section 4 "Scalability and
+ * Extension"): per layer l, k[l] -> bf16 [B, n_kv_heads, prefix_len, head_dim] keys AFTER RoPE,
+ * v[l] -> bf16 [B, n_kv_heads, head_dim, prefix_len] values (key index contiguous).
+ * `k` and `v` themselves are HOST arrays of n_layers device pointers. prefix_len % 8 == 0. */
+typedef struct {
+  const void* const* k;
+  const void* const* v;
+  int32_t prefix_len;
+} dcl_kv;
+
+enum { DCL_DTYPE_F32 = 0, DCL_DTYPE_BF16 = 1 };
+
+/* dcl_denoise_step flags */
+#define DCL_SCORE_ALL_UNCOMMITTED 0x1u  /* score every position p <= i < gen_end, not only masks */
+/* dcl_select_contiguous flags */
+#define DCL_SEL_NO_PROGRESS_GUARD 0x1u  /* literal K: a step with K = 0 commits nothing */
+#define DCL_SEL_SCORE_ALL 0x2u          /* drafts may overwrite non-mask positions (pairs with
+                                           DCL_SCORE_ALL_UNCOMMITTED) */
+
+/* Text for a status code; never NULL. */
+const char* dcl_status_string(dcl_status s);
+
+/* Detail of the last non-OK status returned on this thread (empty string if none). */
+const char* dcl_last_error(void);
+
+/* Validate `cfg` (host) and create a handle. *out receives the handle (host). */
+dcl_status dcl_model_create(const dcl_config* cfg, dcl_model_t* out);
+
+/* Release the handle (host memory only; the weight buffer stays the caller's). NULL is a no-op. */
+void dcl_model_destroy(dcl_model_t model);
+
+/* Bytes of the packed device weight buffer for `cfg`; 0 if `cfg` is invalid. */
+size_t dcl_weights_bytes(const dcl_config* cfg);
+
+/* Pack the model's weights into `dev_buf` (device, `bytes` >= dcl_weights_bytes, 256-byte
+ * aligned). `src` is a HOST array of `n_src` pointers (host or device memory) in this order:
+ *   embed [vocab, d];
+ *   per layer: wq [H*dh, d], wk [Hkv*dh, d], wv [Hkv*dh, d], bq [H*dh], bk [Hkv*dh], bv [Hkv*dh],
+ *              wo [d, H*dh], wgate [F, d], wup [F, d], wdown [d, F], g_attn [d], g_ffn [d];
+ *   g_final [d]; lm_head [vocab, d]
+ * (nn.Linear [out, in] row-major; bias entries may be NULL when qkv_bias = 0), so
+ * n_src = 1 + 12 * n_layers + 2. Elements are `src_dtype` (DCL_DTYPE_F32 or DCL_DTYPE_BF16);
+ * float32 matrices are rounded to bfloat16 (nearest even), vectors are kept in float32.
+ * The handle borrows `dev_buf`, which must outlive it. Synchronises `stream` before returning. */
+dcl_status dcl_load_weights(dcl_model_t model, void* dev_buf, size_t bytes, const void* const* src,
+                            int32_t n_src, int32_t src_dtype, hipStream_t stream);
+
+/* Workspace bytes for a step over B sequences of S tokens (kv_prefix = cached prefix length,
+ * 0 for a full forward); 0 if the arguments are invalid. */
+size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_prefix);
+
+/* Steps (ii) of the iteration: forward over tokens [B, S] (device) and the vocabulary reduction
+ * at the scored rows of each sequence b: x[b,i] == mask_id and p[b] <= i < gen_end (Section 2.1:
+ * probabilities are defined at masked positions), or every p[b] <= i < gen_end with
+ * DCL_SCORE_ALL_UNCOMMITTED. p: device [B]; 0 <= gen_end <= S. Logits are never written to
+ * memory. Token i is at absolute position kv_prefix + i; with kv == NULL the forward covers the
+ * S tokens alone, otherwise they also attend to the cached prefix. Token ids outside
+ * [0, vocab) read an all-zero embedding row. Writes `out` (all B*S rows). ws: device,
+ * ws_bytes >= dcl_workspace_bytes(model, B, S, prefix), 256-byte aligned. */
+dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
+                            const int32_t* p, int32_t gen_end, const dcl_kv* kv, uint32_t flags,
+                            dcl_row_stats out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Steps (iii), (iv) and (i) for every sequence b with p[b] < gen_end, in place on tokens [B, S]
+ * and p [B] (device), using statistics `in` of a dcl_denoise_step on the same tokens:
+ *   L_eff = min(L, gen_end - p);  K = number of leading window rows with conf > tau_commit
+ *   (Eq. compute_k);  K_eff = max(K, 1) unless DCL_SEL_NO_PROGRESS_GUARD (K = 0 would stall
+ *   Algorithm 1; committing the top-1 at p is one sequential step);  x[p, p+K_eff) = top1;
+ *   for j in [p+L, gen_end) with x[j] == mask_id (any x[j] with DCL_SEL_SCORE_ALL) and
+ *   conf[j] > tau_draft: x[j] = top1[j] (Eq. draft_update);  p += K_eff;
+ *   x[p, min(p+L, gen_end)) = mask_id (Eq. remasking for the next iteration).
+ * A window start whose row was not scored (top1 < 0) is never committed. Sequences with
+ * p >= gen_end (or p < 0) are untouched (K_raw = K_eff = 0). K_raw, K_eff: device [B] outputs (may be
+ * NULL). 1 <= L; 0 <= tau_commit <= 1; tau_draft >= 0 (values > 1 disable drafts). */
+dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end,
+                                 int32_t L, float tau_commit, float tau_draft, int32_t mask_id,
+                                 dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,
+                                 hipStream_t stream);
+
+/* Test support: the same forward as dcl_denoise_step, then float32 logits of the rows listed in
+ * `rows` (device [n_rows], flat indices b*S + i) into out (device [n_rows, vocab]). */
+dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
+                            const dcl_kv* kv, const int32_t* rows, int32_t n_rows, float* out,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DCL_H_ */

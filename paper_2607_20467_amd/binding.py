@@ -1,0 +1,258 @@
+"""ctypes binding of libdcl (``include/dcl.h``): same names, argument marshalling only.
+
+Device buffers are torch tensors on ``cuda`` (ROCm); their ``data_ptr()`` and the current
+stream's handle are passed through unchanged. Every step of the computation runs in the
+library's HIP kernels.
+"""
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+DCL_DTYPE_F32, DCL_DTYPE_BF16 = 0, 1
+DCL_SCORE_ALL_UNCOMMITTED = 0x1
+DCL_SEL_NO_PROGRESS_GUARD = 0x1
+DCL_SEL_SCORE_ALL = 0x2
+STATUS = {0: "DCL_OK", 1: "DCL_E_ARG", 2: "DCL_E_UNSUPPORTED", 3: "DCL_E_WORKSPACE", 4: "DCL_E_HIP",
+          5: "DCL_E_STATE"}
+
+
+class DclError(RuntimeError):
+    def __init__(self, status, where, detail):
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+class DclConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("n_layers", "d_model", "n_heads", "n_kv_heads", "head_dim",
+                                              "d_ffn", "vocab", "mask_id")] + \
+               [("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float), ("qkv_bias", ctypes.c_int32),
+                ("rope_enabled", ctypes.c_int32), ("max_positions", ctypes.c_int32)]
+
+
+class DclRowStats(ctypes.Structure):
+    _fields_ = [("top1", ctypes.c_void_p), ("top2", ctypes.c_void_p), ("conf", ctypes.c_void_p),
+                ("p2", ctypes.c_void_p), ("lse", ctypes.c_void_p)]
+
+
+class DclKV(ctypes.Structure):
+    _fields_ = [("k", ctypes.POINTER(ctypes.c_void_p)), ("v", ctypes.POINTER(ctypes.c_void_p)),
+                ("prefix_len", ctypes.c_int32)]
+
+
+def library_path() -> str:
+    return os.path.join(HERE, "libdcl.so")
+
+
+_lib = None
+
+
+def load_library():
+    """Load libdcl.so; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    vp, i32, u32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float, ctypes.c_size_t
+    sig = {
+        "dcl_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "dcl_last_error": (ctypes.c_char_p, []),
+        "dcl_model_create": (ctypes.c_int, [ctypes.POINTER(DclConfig), ctypes.POINTER(vp)]),
+        "dcl_model_destroy": (None, [vp]),
+        "dcl_weights_bytes": (sz, [ctypes.POINTER(DclConfig)]),
+        "dcl_load_weights": (ctypes.c_int, [vp, vp, sz, ctypes.POINTER(vp), i32, i32, vp]),
+        "dcl_workspace_bytes": (sz, [vp, i32, i32, i32]),
+        "dcl_denoise_step": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, DclRowStats,
+                                            vp, sz, vp]),
+        "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, f32, f32, i32, DclRowStats, vp, vp,
+                                                 u32, vp]),
+        "dcl_debug_logits": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, i32, vp, vp, sz, vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status, where):
+    if status != 0:
+        raise DclError(status, where, dcl_last_error())
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+# ---------------------------------------------------------------- one function per C entry point
+
+def dcl_status_string(status: int) -> str:
+    return load_library().dcl_status_string(status).decode()
+
+
+def dcl_last_error() -> str:
+    return load_library().dcl_last_error().decode()
+
+
+def dcl_model_create(cfg: DclConfig) -> int:
+    h = ctypes.c_void_p()
+    _check(load_library().dcl_model_create(ctypes.byref(cfg), ctypes.byref(h)), "dcl_model_create")
+    return h.value
+
+
+def dcl_model_destroy(model: int) -> None:
+    load_library().dcl_model_destroy(model)
+
+
+def dcl_weights_bytes(cfg: DclConfig) -> int:
+    return load_library().dcl_weights_bytes(ctypes.byref(cfg))
+
+
+def dcl_load_weights(model: int, dev_buf, nbytes: int, src_ptrs: Sequence[Optional[int]], src_dtype: int,
+                     stream=None) -> None:
+    arr = (ctypes.c_void_p * len(src_ptrs))(*src_ptrs)
+    _check(load_library().dcl_load_weights(model, _ptr(dev_buf), nbytes, arr, len(src_ptrs), src_dtype,
+                                           _stream(stream)), "dcl_load_weights")
+
+
+def dcl_workspace_bytes(model: int, B: int, S: int, kv_prefix: int = 0) -> int:
+    return load_library().dcl_workspace_bytes(model, B, S, kv_prefix)
+
+
+def _stats(st) -> DclRowStats:
+    return DclRowStats(*(_ptr(st[k]) for k in ("top1", "top2", "conf", "p2", "lse")))
+
+
+def _kv(kv):
+    """kv: None or (list of per-layer K tensors, list of per-layer V tensors, prefix_len)."""
+    if kv is None:
+        return None, None
+    ks, vs, P = kv
+    ka = (ctypes.c_void_p * len(ks))(*[_ptr(t) for t in ks])
+    va = (ctypes.c_void_p * len(vs))(*[_ptr(t) for t in vs])
+    s = DclKV(ctypes.cast(ka, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(va, ctypes.POINTER(ctypes.c_void_p)), P)
+    return ctypes.byref(s), (s, ka, va)
+
+
+def dcl_denoise_step(model: int, tokens, B: int, S: int, p, gen_end: int, kv, flags: int, stats, ws, ws_bytes: int,
+                     stream=None) -> None:
+    kvp, keep = _kv(kv)
+    _check(load_library().dcl_denoise_step(model, _ptr(tokens), B, S, _ptr(p), gen_end, kvp, flags, _stats(stats),
+                                           _ptr(ws), ws_bytes, _stream(stream)), "dcl_denoise_step")
+    del keep
+
+
+def dcl_select_contiguous(tokens, B: int, S: int, p, gen_end: int, L: int, tau_commit: float, tau_draft: float,
+                          mask_id: int, stats, k_raw=None, k_eff=None, flags: int = 0, stream=None) -> None:
+    _check(load_library().dcl_select_contiguous(_ptr(tokens), B, S, _ptr(p), gen_end, L, tau_commit, tau_draft,
+                                                mask_id, _stats(stats), _ptr(k_raw), _ptr(k_eff), flags,
+                                                _stream(stream)), "dcl_select_contiguous")
+
+
+def dcl_debug_logits(model: int, tokens, B: int, S: int, kv, rows, n_rows: int, out, ws, ws_bytes: int,
+                     stream=None) -> None:
+    kvp, keep = _kv(kv)
+    _check(load_library().dcl_debug_logits(model, _ptr(tokens), B, S, kvp, _ptr(rows), n_rows, _ptr(out), _ptr(ws),
+                                           ws_bytes, _stream(stream)), "dcl_debug_logits")
+    del keep
+
+
+# ---------------------------------------------------------------- convenience owner of device buffers
+
+def config_from_geometry(g, max_positions: int = 4096, rope_enabled: bool = True) -> DclConfig:
+    """DclConfig from any object with the geometry fields (e.g. ``synth.Geometry``)."""
+    return DclConfig(g.n_layers, g.d_model, g.n_heads, g.n_kv_heads, g.head_dim, g.d_ffn, g.vocab, g.mask_id,
+                     g.rms_eps, g.rope_base, int(g.qkv_bias), int(rope_enabled), max_positions)
+
+
+class Runner:
+    """Owns a model handle plus torch-allocated weight buffer, workspace and statistics buffers."""
+
+    def __init__(self, geom, tensors, max_positions: int = 4096, rope_enabled: bool = True, stream=None):
+        """tensors: sequence of numpy arrays / torch tensors (or None for absent biases) in the load order of
+        ``include/dcl.h``; float32 or bfloat16 bit patterns (uint16 / int16 / torch.bfloat16)."""
+        import numpy as np
+        import torch
+        self.torch = torch
+        self.geom = geom
+        self.cfg = config_from_geometry(geom, max_positions, rope_enabled)
+        self.model = dcl_model_create(self.cfg)
+        nbytes = dcl_weights_bytes(self.cfg)
+        self.wbuf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        dtype = None
+        keep, ptrs = [], []
+        for t in tensors:
+            if t is None:
+                ptrs.append(None)
+                continue
+            if isinstance(t, np.ndarray):
+                t = torch.from_numpy(np.ascontiguousarray(t))
+            t = t.contiguous()
+            dt = DCL_DTYPE_F32 if t.dtype == torch.float32 else DCL_DTYPE_BF16
+            if dtype is None:
+                dtype = dt
+            elif dt != dtype and t.dim() > 1:
+                raise ValueError("all weight matrices must share one dtype")
+            if dt != dtype:  # vectors follow the matrices' dtype
+                t = t.float() if dtype == DCL_DTYPE_F32 else t.view(torch.int16)
+            keep.append(t)
+            ptrs.append(t.data_ptr())
+        dcl_load_weights(self.model, self.wbuf, nbytes, ptrs, dtype, stream)
+        del keep
+        self.ws = None
+        self.ws_key = None
+
+    def workspace(self, B, S, P=0):
+        need = dcl_workspace_bytes(self.model, B, S, P)
+        if self.ws is None or self.ws.numel() < need:
+            self.ws = self.torch.empty(need, dtype=self.torch.uint8, device="cuda")
+        return self.ws, need
+
+    def new_stats(self, B, S):
+        t = self.torch
+        return {"top1": t.empty((B, S), dtype=t.int32, device="cuda"),
+                "top2": t.empty((B, S), dtype=t.int32, device="cuda"),
+                "conf": t.empty((B, S), dtype=t.float32, device="cuda"),
+                "p2": t.empty((B, S), dtype=t.float32, device="cuda"),
+                "lse": t.empty((B, S), dtype=t.float32, device="cuda")}
+
+    def step(self, tokens, p, gen_end, stats=None, kv=None, flags=0, stream=None):
+        B, S = tokens.shape
+        ws, n = self.workspace(B, S, 0 if kv is None else kv[2])
+        if stats is None:
+            stats = self.new_stats(B, S)
+        dcl_denoise_step(self.model, tokens, B, S, p, gen_end, kv, flags, stats, ws, n, stream)
+        return stats
+
+    def logits(self, tokens, rows, kv=None, stream=None):
+        B, S = tokens.shape
+        ws, n = self.workspace(B, S, 0 if kv is None else kv[2])
+        out = self.torch.empty((rows.numel(), self.geom.vocab), dtype=self.torch.float32, device="cuda")
+        dcl_debug_logits(self.model, tokens, B, S, kv, rows, rows.numel(), out, ws, n, stream)
+        return out
+
+    def close(self):
+        if self.model:
+            dcl_model_destroy(self.model)
+            self.model = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,401 @@
+// C-ABI entry points of libdcl: argument checks, packed-weight and workspace layouts, and the
+// launch sequence of one denoising iteration (all asynchronous on the caller's stream).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "dcl_internal.h"
+
+using namespace dcl;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+dcl_status fail(dcl_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+dcl_status hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(DCL_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  return DCL_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+dcl_status check_config(const dcl_config* c) {
+  if (!c) return fail(DCL_E_ARG, "config is NULL");
+  if (c->n_layers < 1 || c->n_layers > 512) return fail(DCL_E_ARG, "n_layers %d outside [1, 512]", c->n_layers);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(DCL_E_UNSUPPORTED, "head_dim %d: kernels exist for 64 and 128", c->head_dim);
+  if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads != 0)
+    return fail(DCL_E_UNSUPPORTED, "n_heads %d must be a positive multiple of n_kv_heads %d", c->n_heads,
+                c->n_kv_heads);
+  if (c->d_model < 16 || c->d_model % 16 != 0) return fail(DCL_E_UNSUPPORTED, "d_model %d must be a multiple of 16", c->d_model);
+  if (c->d_ffn < 16 || c->d_ffn % 16 != 0) return fail(DCL_E_UNSUPPORTED, "d_ffn %d must be a multiple of 16", c->d_ffn);
+  if ((long)c->n_heads * c->head_dim > (1 << 20)) return fail(DCL_E_ARG, "n_heads * head_dim too large");
+  if (c->vocab < 2) return fail(DCL_E_ARG, "vocab %d < 2", c->vocab);
+  if (c->mask_id < 0 || c->mask_id >= c->vocab) return fail(DCL_E_ARG, "mask_id %d outside [0, vocab)", c->mask_id);
+  if (!(c->rms_eps > 0.f) || !isfinite(c->rms_eps)) return fail(DCL_E_ARG, "rms_eps must be > 0");
+  if (!(c->rope_base > 1.f) || !isfinite(c->rope_base)) return fail(DCL_E_ARG, "rope_base must be > 1");
+  if (c->max_positions < 1 || c->max_positions > 65536)
+    return fail(DCL_E_ARG, "max_positions %d outside [1, 65536]", c->max_positions);
+  if (c->qkv_bias != 0 && c->qkv_bias != 1) return fail(DCL_E_ARG, "qkv_bias must be 0 or 1");
+  if (c->rope_enabled != 0 && c->rope_enabled != 1) return fail(DCL_E_ARG, "rope_enabled must be 0 or 1");
+  return DCL_OK;
+}
+
+WeightLayout make_layout(const dcl_config& c) {
+  WeightLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t d = c.d_model, V = c.vocab, F = c.d_ffn, dh = c.head_dim;
+  const size_t qkv = (size_t)(c.n_heads + 2 * c.n_kv_heads) * dh, hd = (size_t)c.n_heads * dh;
+  L.embed = take(V * d * 2);
+  for (int l = 0; l < c.n_layers; ++l) {
+    LayerOffsets& o = L.layer[l];
+    o.wqkv = take(qkv * d * 2);
+    o.bqkv = take(qkv * 4);
+    o.wo = take(d * hd * 2);
+    o.wgu = take(2 * F * d * 2);
+    o.wd = take(d * F * 2);
+    o.g1 = take(d * 4);
+    o.g2 = take(d * 4);
+  }
+  L.gf = take(d * 4);
+  L.lm = take(V * d * 2);
+  L.rope = take((size_t)c.max_positions * (dh / 2) * 8);
+  L.total = off;
+  return L;
+}
+
+StepLayout step_layout(const dcl_config& c, int B, int S) {
+  StepLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t T = (size_t)B * S, d = c.d_model, dh = c.head_dim;
+  L.T = (int)T;
+  L.S = S;
+  L.Sp = (S + 7) / 8 * 8;
+  L.n_vt = (c.vocab + kLmTile - 1) / kLmTile;
+  L.r = take(T * d * 4);
+  L.u = take(T * d * 2);
+  L.q = take(T * c.n_heads * dh * 2);
+  L.k = take(T * c.n_kv_heads * dh * 2);
+  L.vt = take((size_t)B * c.n_kv_heads * dh * L.Sp * 2);
+  L.o = take(T * c.n_heads * dh * 2);
+  L.a = take(T * c.d_ffn * 2);
+  L.rows = take(T * 4);
+  L.count = take(4);
+  L.hf = take(T * d * 2);
+  const size_t np = T * L.n_vt * 4;
+  L.pm1 = take(np);
+  L.pi1 = take(np);
+  L.pm2 = take(np);
+  L.pi2 = take(np);
+  L.ps = take(np);
+  L.total = off;
+  return L;
+}
+
+template <class T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off);
+}
+
+dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv, void* ws,
+                           size_t ws_bytes) {
+  if (!m) return fail(DCL_E_ARG, "model is NULL");
+  if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
+  if (!tokens) return fail(DCL_E_ARG, "tokens is NULL");
+  if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
+  if ((long)B * S > (1 << 22)) return fail(DCL_E_ARG, "B*S = %ld too large", (long)B * S);
+  const int P = kv ? kv->prefix_len : 0;
+  if (kv) {
+    if (!kv->k || !kv->v) return fail(DCL_E_ARG, "kv->k / kv->v is NULL");
+    if (P < 0 || P % 8 != 0) return fail(DCL_E_UNSUPPORTED, "kv prefix_len %d must be a non-negative multiple of 8", P);
+    for (int l = 0; l < m->cfg.n_layers; ++l)
+      if (P > 0 && (!kv->k[l] || !kv->v[l])) return fail(DCL_E_ARG, "kv cache pointer of layer %d is NULL", l);
+  }
+  if ((long)P + S > m->cfg.max_positions)
+    return fail(DCL_E_ARG, "positions up to %ld exceed max_positions %d", (long)P + S, m->cfg.max_positions);
+  if (!ws) return fail(DCL_E_ARG, "workspace is NULL");
+  if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(DCL_E_ARG, "workspace must be 256-byte aligned");
+  const size_t need = step_layout(m->cfg, B, S).total;
+  if (ws_bytes < need) return fail(DCL_E_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
+  return DCL_OK;
+}
+
+// a2-a7: embedding and every transformer layer; leaves the residual stream in ws.r.
+void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_kv* kv, void* ws,
+                 const StepLayout& L, hipStream_t s) {
+  const dcl_config& c = m->cfg;
+  const int T = B * S, d = c.d_model, dh = c.head_dim;
+  const int P = kv ? kv->prefix_len : 0;
+  void* wb = m->wbuf;
+  float* r = at<float>(ws, L.r);
+  bf16_t* u = at<bf16_t>(ws, L.u);
+  bf16_t* a = at<bf16_t>(ws, L.a);
+  bf16_t* o = at<bf16_t>(ws, L.o);
+  launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, s);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const LayerOffsets& lo = m->lay.layer[l];
+    launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, s);
+    QkvOut qo;
+    qo.q = at<bf16_t>(ws, L.q);
+    qo.k = at<bf16_t>(ws, L.k);
+    qo.vt = at<bf16_t>(ws, L.vt);
+    qo.bias = c.qkv_bias ? at<float>(wb, lo.bqkv) : nullptr;
+    qo.rope = c.rope_enabled ? at<float2>(wb, m->lay.rope) : nullptr;
+    qo.H = c.n_heads;
+    qo.Hkv = c.n_kv_heads;
+    qo.dh = dh;
+    qo.S = S;
+    qo.Sp = L.Sp;
+    qo.pos0 = P;
+    gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
+    AttnArgs aa;
+    aa.q = qo.q;
+    aa.k = qo.k;
+    aa.vt = qo.vt;
+    aa.kc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->k[l]) : nullptr;
+    aa.vc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->v[l]) : nullptr;
+    aa.o = o;
+    aa.B = B;
+    aa.H = c.n_heads;
+    aa.Hkv = c.n_kv_heads;
+    aa.dh = dh;
+    aa.S = S;
+    aa.Sp = L.Sp;
+    aa.P = P;
+    aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
+    launch_attention(aa, s);
+    gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, s);
+    launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, s);
+    gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
+    gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, s);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dcl_status_string(dcl_status s) {
+  switch (s) {
+    case DCL_OK: return "ok";
+    case DCL_E_ARG: return "invalid argument";
+    case DCL_E_UNSUPPORTED: return "unsupported geometry";
+    case DCL_E_WORKSPACE: return "buffer too small";
+    case DCL_E_HIP: return "HIP error";
+    case DCL_E_STATE: return "invalid state";
+  }
+  return "unknown status";
+}
+
+const char* dcl_last_error(void) { return g_err; }
+
+dcl_status dcl_model_create(const dcl_config* cfg, dcl_model_t* out) {
+  if (!out) return fail(DCL_E_ARG, "out is NULL");
+  *out = nullptr;
+  dcl_status st = check_config(cfg);
+  if (st != DCL_OK) return st;
+  Model* m = new (std::nothrow) Model();
+  if (!m) return fail(DCL_E_ARG, "out of host memory");
+  m->cfg = *cfg;
+  m->lay = make_layout(*cfg);
+  *out = reinterpret_cast<dcl_model_t>(m);
+  return DCL_OK;
+}
+
+void dcl_model_destroy(dcl_model_t model) { delete reinterpret_cast<Model*>(model); }
+
+size_t dcl_weights_bytes(const dcl_config* cfg) {
+  if (check_config(cfg) != DCL_OK) return 0;
+  return make_layout(*cfg).total;
+}
+
+dcl_status dcl_load_weights(dcl_model_t model, void* dev_buf, size_t bytes, const void* const* src, int32_t n_src,
+                            int32_t src_dtype, hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  if (!m) return fail(DCL_E_ARG, "model is NULL");
+  if (!dev_buf || !src) return fail(DCL_E_ARG, "dev_buf / src is NULL");
+  if ((reinterpret_cast<uintptr_t>(dev_buf) & 255) != 0) return fail(DCL_E_ARG, "dev_buf must be 256-byte aligned");
+  if (bytes < m->lay.total) return fail(DCL_E_WORKSPACE, "weight buffer %zu bytes < required %zu", bytes, m->lay.total);
+  if (src_dtype != DCL_DTYPE_F32 && src_dtype != DCL_DTYPE_BF16) return fail(DCL_E_ARG, "src_dtype %d", src_dtype);
+  const dcl_config& c = m->cfg;
+  const int expect = 1 + 12 * c.n_layers + 2;
+  if (n_src != expect) return fail(DCL_E_ARG, "n_src %d, expected %d", n_src, expect);
+  for (int i = 0; i < n_src; ++i) {
+    const int li = (i - 1) % 12;
+    const bool is_bias = i >= 1 && i < 1 + 12 * c.n_layers && li >= 3 && li <= 5;
+    if (!src[i] && !(is_bias && !c.qkv_bias)) return fail(DCL_E_ARG, "src[%d] is NULL", i);
+  }
+  const size_t es = src_dtype == DCL_DTYPE_F32 ? 4 : 2;
+  const size_t d = c.d_model, V = c.vocab, F = c.d_ffn, dh = c.head_dim, H = c.n_heads, Hkv = c.n_kv_heads;
+  size_t biggest = V * d;
+  if (F * d > biggest) biggest = F * d;
+  if (H * dh * d > biggest) biggest = H * dh * d;
+  void* stage = nullptr;
+  dcl_status st = hip_check(hipMalloc(&stage, biggest * es), "hipMalloc(staging)");
+  if (st != DCL_OK) return st;
+  void* wb = dev_buf;
+  auto put_mat = [&](const void* p, size_t rows, size_t cols, size_t dst_off, int mode, int dst_row0) -> dcl_status {
+    dcl_status e = hip_check(hipMemcpyAsync(stage, p, rows * cols * es, hipMemcpyDefault, stream), "hipMemcpyAsync");
+    if (e != DCL_OK) return e;
+    launch_pack_rows(stage, src_dtype, at<bf16_t>(wb, dst_off), (int)rows, (int)cols, mode, (int)dh, dst_row0, stream);
+    return hip_check(hipGetLastError(), "pack_rows launch");
+  };
+  auto put_vec = [&](const void* p, size_t n, size_t dst_off, int mode, int dst0) -> dcl_status {
+    if (p) {
+      dcl_status e = hip_check(hipMemcpyAsync(stage, p, n * es, hipMemcpyDefault, stream), "hipMemcpyAsync");
+      if (e != DCL_OK) return e;
+    }
+    launch_pack_vec(p ? stage : nullptr, src_dtype, at<float>(wb, dst_off), (int)n, mode, (int)dh, dst0, stream);
+    return hip_check(hipGetLastError(), "pack_vec launch");
+  };
+#define TRY(x)            \
+  do {                    \
+    st = (x);             \
+    if (st != DCL_OK) {   \
+      (void)hipFree(stage); \
+      return st;          \
+    }                     \
+  } while (0)
+  TRY(put_mat(src[0], V, d, m->lay.embed, 0, 0));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const void* const* s = src + 1 + 12 * l;
+    const LayerOffsets& lo = m->lay.layer[l];
+    TRY(put_mat(s[0], H * dh, d, lo.wqkv, 1, 0));
+    TRY(put_mat(s[1], Hkv * dh, d, lo.wqkv, 1, (int)(H * dh)));
+    TRY(put_mat(s[2], Hkv * dh, d, lo.wqkv, 0, (int)((H + Hkv) * dh)));
+    TRY(put_vec(c.qkv_bias ? s[3] : nullptr, H * dh, lo.bqkv, 1, 0));
+    TRY(put_vec(c.qkv_bias ? s[4] : nullptr, Hkv * dh, lo.bqkv, 1, (int)(H * dh)));
+    TRY(put_vec(c.qkv_bias ? s[5] : nullptr, Hkv * dh, lo.bqkv, 0, (int)((H + Hkv) * dh)));
+    TRY(put_mat(s[6], d, H * dh, lo.wo, 0, 0));
+    TRY(put_mat(s[7], F, d, lo.wgu, 2, 0));
+    TRY(put_mat(s[8], F, d, lo.wgu, 3, 0));
+    TRY(put_mat(s[9], d, F, lo.wd, 0, 0));
+    TRY(put_vec(s[10], d, lo.g1, 0, 0));
+    TRY(put_vec(s[11], d, lo.g2, 0, 0));
+  }
+  TRY(put_vec(src[1 + 12 * c.n_layers], d, m->lay.gf, 0, 0));
+  TRY(put_mat(src[2 + 12 * c.n_layers], V, d, m->lay.lm, 0, 0));
+#undef TRY
+  // RoPE table: theta = pos * base^(-2i/dh), built in float64 on the host, stored as float32 (cos, sin).
+  const size_t half = dh / 2, npos = (size_t)c.max_positions;
+  std::vector<float> tab(npos * half * 2);
+  for (size_t pos = 0; pos < npos; ++pos)
+    for (size_t i = 0; i < half; ++i) {
+      const double inv_freq = pow((double)c.rope_base, -(2.0 * (double)i) / (double)dh);
+      const double ang = (double)pos * inv_freq;
+      tab[(pos * half + i) * 2] = (float)cos(ang);
+      tab[(pos * half + i) * 2 + 1] = (float)sin(ang);
+    }
+  st = hip_check(hipMemcpyAsync(at<char>(wb, m->lay.rope), tab.data(), tab.size() * 4, hipMemcpyHostToDevice, stream),
+                 "hipMemcpyAsync(rope)");
+  dcl_status st2 = hip_check(hipStreamSynchronize(stream), "hipStreamSynchronize(load)");
+  (void)hipFree(stage);
+  if (st != DCL_OK) return st;
+  if (st2 != DCL_OK) return st2;
+  m->wbuf = dev_buf;
+  m->loaded = true;
+  return DCL_OK;
+}
+
+size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_prefix) {
+  Model* m = reinterpret_cast<Model*>(model);
+  if (!m || B < 1 || S < 1 || kv_prefix < 0 || (long)B * S > (1 << 22)) return 0;
+  return step_layout(m->cfg, B, S).total;
+}
+
+dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S, const int32_t* p,
+                            int32_t gen_end, const dcl_kv* kv, uint32_t flags, dcl_row_stats out, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  dcl_status st = check_step_args(m, tokens, B, S, kv, ws, ws_bytes);
+  if (st != DCL_OK) return st;
+  if (!p) return fail(DCL_E_ARG, "p is NULL");
+  if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
+  if (flags & ~(uint32_t)DCL_SCORE_ALL_UNCOMMITTED) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  if (!out.top1 || !out.top2 || !out.conf || !out.p2 || !out.lse) return fail(DCL_E_ARG, "an output array is NULL");
+  const dcl_config& c = m->cfg;
+  const StepLayout L = step_layout(c, B, S);
+  (void)hipGetLastError();  // clear a stale error so the check below reports this call's launches
+  run_forward(m, tokens, B, S, kv, ws, L, stream);
+  int32_t* rows = at<int32_t>(ws, L.rows);
+  int32_t* count = at<int32_t>(ws, L.count);
+  launch_compact(tokens, p, B, S, gen_end, c.mask_id, (flags & DCL_SCORE_ALL_UNCOMMITTED) ? 1 : 0, rows, count, out,
+                 stream);
+  bf16_t* hf = at<bf16_t>(ws, L.hf);
+  launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count, stream);
+  LmOut lo;
+  lo.pm1 = at<float>(ws, L.pm1);
+  lo.pi1 = at<int32_t>(ws, L.pi1);
+  lo.pm2 = at<float>(ws, L.pm2);
+  lo.pi2 = at<int32_t>(ws, L.pi2);
+  lo.ps = at<float>(ws, L.ps);
+  lo.n_vt = L.n_vt;
+  lo.count = count;
+  gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
+  launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, L.T, out, stream);
+  return hip_check(hipGetLastError(), "denoise_step launch");
+}
+
+dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end, int32_t L,
+                                 float tau_commit, float tau_draft, int32_t mask_id, dcl_row_stats in,
+                                 int32_t* K_raw, int32_t* K_eff, uint32_t flags, hipStream_t stream) {
+  if (!tokens || !p) return fail(DCL_E_ARG, "tokens / p is NULL");
+  if (!in.top1 || !in.conf) return fail(DCL_E_ARG, "in.top1 / in.conf is NULL");
+  if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
+  if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
+  if (L < 1) return fail(DCL_E_ARG, "window L=%d must be >= 1", L);
+  if (!(tau_commit >= 0.f && tau_commit <= 1.f)) return fail(DCL_E_ARG, "tau_commit %g outside [0, 1]", tau_commit);
+  if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
+  if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL)) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  (void)hipGetLastError();
+  launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, in, K_raw, K_eff, flags, stream);
+  return hip_check(hipGetLastError(), "select launch");
+}
+
+dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv,
+                            const int32_t* rows, int32_t n_rows, float* out, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  dcl_status st = check_step_args(m, tokens, B, S, kv, ws, ws_bytes);
+  if (st != DCL_OK) return st;
+  if (!rows || !out) return fail(DCL_E_ARG, "rows / out is NULL");
+  if (n_rows < 1 || n_rows > B * S) return fail(DCL_E_ARG, "n_rows %d outside [1, B*S]", n_rows);
+  const dcl_config& c = m->cfg;
+  const StepLayout L = step_layout(c, B, S);
+  (void)hipGetLastError();
+  run_forward(m, tokens, B, S, kv, ws, L, stream);
+  int32_t* count = at<int32_t>(ws, L.count);
+  st = hip_check(hipMemcpyAsync(count, &n_rows, 4, hipMemcpyHostToDevice, stream), "hipMemcpyAsync(count)");
+  if (st != DCL_OK) return st;
+  // the host value must stay alive until the copy ran
+  st = hip_check(hipStreamSynchronize(stream), "hipStreamSynchronize(debug)");
+  if (st != DCL_OK) return st;
+  bf16_t* hf = at<bf16_t>(ws, L.hf);
+  launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count, stream);
+  gemm_store_f32(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, n_rows, c.d_model, out, stream);
+  return hip_check(hipGetLastError(), "debug_logits launch");
+}
+
+}  // extern "C"

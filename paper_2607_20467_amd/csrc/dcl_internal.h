@@ -1,0 +1,96 @@
+// Internal declarations of libdcl: device helpers, the model handle, kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dcl.h"
+
+namespace dcl {
+
+typedef uint16_t bf16_t;  // bfloat16 bit pattern
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// float -> bfloat16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u) return (bf16_t)((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// Packed-weight layout (byte offsets into the caller's weight buffer).
+struct LayerOffsets {
+  size_t wqkv, bqkv, wo, wgu, wd, g1, g2;
+};
+struct WeightLayout {
+  size_t embed, gf, lm, rope, total;
+  LayerOffsets layer[512];
+};
+
+struct Model {
+  dcl_config cfg;
+  WeightLayout lay;
+  void* wbuf = nullptr;  // borrowed
+  bool loaded = false;
+  int qkv_rows() const { return (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim; }
+};
+
+// Step workspace layout.
+struct StepLayout {
+  size_t r, u, q, k, vt, o, a, rows, count, hf, pm1, pi1, pm2, pi2, ps, total;
+  int T, S, Sp, n_vt;
+};
+
+// Vocabulary tile of the fused LM-head reduction (vocab ids per partial).
+constexpr int kLmTile = 128;
+
+// ---------------------------------------------------------------- launchers (stream-ordered)
+void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, hipStream_t s);
+void launch_rmsnorm(const float* r, const float* g, bf16_t* u, int T, int d, float eps,
+                    const int32_t* rows, const int32_t* count, hipStream_t s);
+void launch_compact(const int32_t* tokens, const int32_t* p, int B, int S, int gen_end, int mask_id,
+                    int score_all, int32_t* rows, int32_t* count, dcl_row_stats st, hipStream_t s);
+void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const int32_t* pi2,
+                  const float* ps, int n_vt, const int32_t* rows, const int32_t* count, int max_rows,
+                  dcl_row_stats st, hipStream_t s);
+void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c,
+                   float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
+                   uint32_t flags, hipStream_t s);
+void launch_pack_rows(const void* src, int src_dtype, bf16_t* dst, int rows, int cols, int mode,
+                      int dh, int dst_row0, hipStream_t s);
+void launch_pack_vec(const void* src, int src_dtype, float* dst, int n, int mode, int dh, int dst0,
+                     hipStream_t s);
+
+// GEMM family: C[w, t] = sum_k W[w, k] X[t, k], W bf16 [Nw, K], X bf16 [T, K] (both K-contiguous).
+struct QkvOut {
+  bf16_t *q, *k, *vt;
+  const float* bias;     // packed order, or null
+  const float2* rope;    // [max_pos, dh/2] (cos, sin) or null (RoPE off)
+  int H, Hkv, dh, S, Sp, pos0;
+};
+struct LmOut {
+  float *pm1, *pm2, *ps;
+  int32_t *pi1, *pi2;
+  int n_vt;
+  const int32_t* count;  // number of valid X rows (device)
+};
+void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, hipStream_t s);
+void gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, hipStream_t s);
+void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, hipStream_t s);
+void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, hipStream_t s);
+void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, hipStream_t s);
+
+// Non-causal attention over [cache (P keys) || fresh (S keys)].
+struct AttnArgs {
+  const bf16_t *q, *k, *vt;      // [B,H,S,dh], [B,Hkv,S,dh], [B,Hkv,dh,Sp]
+  const bf16_t *kc, *vc;         // [B,Hkv,P,dh], [B,Hkv,dh,P] or null
+  bf16_t* o;                     // [B,S,H*dh]
+  int B, H, Hkv, dh, S, Sp, P;
+  float scale_log2;              // log2(e) / sqrt(dh)
+};
+void launch_attention(const AttnArgs& a, hipStream_t s);
+
+}  // namespace dcl

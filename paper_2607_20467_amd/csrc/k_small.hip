@@ -1,0 +1,313 @@
+// Memory-bound kernels of the denoising step: embedding gather, RMSNorm, scored-row compaction,
+// merge of the fused LM-head partials, DCV + draft selection, weight packing.
+#include <float.h>
+#include <limits.h>
+
+#include "dcl_internal.h"
+
+namespace dcl {
+
+// ---------------------------------------------------------------- embedding gather
+// r[t, :] = E[tokens[t], :] widened to float32; ids outside [0, V) give a zero row.
+__global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ tokens,
+                                                   const bf16_t* __restrict__ E, float* __restrict__ r,
+                                                   int T, int d, int V) {
+  const int chunks = d / 8;
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)T * chunks) return;
+  int t = (int)(idx / chunks), c = (int)(idx % chunks);
+  int id = tokens[t];
+  float4 lo = {0.f, 0.f, 0.f, 0.f}, hi = lo;
+  if (id >= 0 && id < V) {
+    uint4 v = *reinterpret_cast<const uint4*>(E + (size_t)id * d + c * 8);
+    lo = {__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u),
+          __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u)};
+    hi = {__uint_as_float(v.z << 16), __uint_as_float(v.z & 0xFFFF0000u),
+          __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xFFFF0000u)};
+  }
+  float4* dst = reinterpret_cast<float4*>(r + (size_t)t * d + c * 8);
+  dst[0] = lo;
+  dst[1] = hi;
+}
+
+void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, hipStream_t s) {
+  long n = (long)T * (d / 8);
+  if (n == 0) return;
+  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tokens, E, r, T, d, V);
+}
+
+// ---------------------------------------------------------------- RMSNorm
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// One wavefront per row: u = bf16(r * rsqrt(mean(r^2) + eps) * g). With `rows`, output row j
+// normalises input row rows[j] (j < *count); otherwise output row j = input row j (j < T).
+// T is also the number of rows of r.
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ r, const float* __restrict__ g,
+                                                     bf16_t* __restrict__ u, int T, int d, float eps,
+                                                     const int32_t* __restrict__ rows,
+                                                     const int32_t* __restrict__ count) {
+  int lane = threadIdx.x & 63;
+  int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  int n = rows ? *count : T;
+  if (j >= n) return;
+  int src = rows ? rows[j] : j;
+  bf16_t* y = u + (size_t)j * d;
+  if (src < 0 || src >= T) {  // row index outside the residual buffer: zero row
+    for (int c = lane * 4; c < d; c += 256) *reinterpret_cast<uint2*>(y + c) = make_uint2(0, 0);
+    return;
+  }
+  const float* x = r + (size_t)src * d;
+  float ss = 0.f;
+  for (int c = lane * 4; c < d; c += 256) {
+    float4 v = *reinterpret_cast<const float4*>(x + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int c = lane * 4; c < d; c += 256) {
+    float4 v = *reinterpret_cast<const float4*>(x + c);
+    float4 w = *reinterpret_cast<const float4*>(g + c);
+    uint2 o;
+    o.x = (uint32_t)f2bf(v.x * inv * w.x) | ((uint32_t)f2bf(v.y * inv * w.y) << 16);
+    o.y = (uint32_t)f2bf(v.z * inv * w.z) | ((uint32_t)f2bf(v.w * inv * w.w) << 16);
+    *reinterpret_cast<uint2*>(y + c) = o;
+  }
+}
+
+void launch_rmsnorm(const float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
+                    const int32_t* count, hipStream_t s) {
+  if (T == 0) return;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((T + 3) / 4), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+}
+
+// ---------------------------------------------------------------- scored-row compaction
+// Single workgroup: rows = flat indices b*S+i of scored positions in increasing order, count = R.
+// Unscored positions get the sentinel statistics.
+__global__ void __launch_bounds__(1024) compact_kernel(const int32_t* __restrict__ tokens,
+                                                      const int32_t* __restrict__ p, int B, int S,
+                                                      int gen_end, int mask_id, int score_all,
+                                                      int32_t* __restrict__ rows, int32_t* __restrict__ count,
+                                                      dcl_row_stats st) {
+  __shared__ int wave_tot[16];
+  __shared__ int base;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  if (tid == 0) base = 0;
+  __syncthreads();
+  const int total = B * S;
+  for (int start = 0; start < total; start += 1024) {
+    int idx = start + tid;
+    int flag = 0;
+    if (idx < total) {
+      int b = idx / S, i = idx % S;
+      flag = (i >= p[b] && i < gen_end && (score_all || tokens[idx] == mask_id)) ? 1 : 0;
+      if (!flag) {
+        st.top1[idx] = -1;
+        st.top2[idx] = -1;
+        st.conf[idx] = -1.f;
+        st.p2[idx] = -1.f;
+        st.lse[idx] = 0.f;
+      }
+    }
+    unsigned long long m = __ballot(flag);
+    int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_tot[wid] = __popcll(m);
+    __syncthreads();
+    int off = base;
+    for (int w = 0; w < wid; ++w) off += wave_tot[w];
+    if (flag) rows[off + before] = idx;
+    __syncthreads();
+    if (tid == 0) {
+      int add = 0;
+      for (int w = 0; w < 16; ++w) add += wave_tot[w];
+      base += add;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) *count = base;
+}
+
+void launch_compact(const int32_t* tokens, const int32_t* p, int B, int S, int gen_end, int mask_id,
+                    int score_all, int32_t* rows, int32_t* count, dcl_row_stats st, hipStream_t s) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, tokens, p, B, S, gen_end, mask_id, score_all,
+                     rows, count, st);
+}
+
+// ---------------------------------------------------------------- top-2 / sum-exp merge
+struct Top2 {
+  float m1, m2;
+  int i1, i2;
+};
+// (value desc, id asc) ordering
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+__device__ __forceinline__ Top2 top2_merge(Top2 a, Top2 b) {
+  Top2 o;
+  if (better(a.m1, a.i1, b.m1, b.i1)) {
+    o.m1 = a.m1; o.i1 = a.i1;
+    if (better(a.m2, a.i2, b.m1, b.i1)) { o.m2 = a.m2; o.i2 = a.i2; } else { o.m2 = b.m1; o.i2 = b.i1; }
+  } else {
+    o.m1 = b.m1; o.i1 = b.i1;
+    if (better(b.m2, b.i2, a.m1, a.i1)) { o.m2 = b.m2; o.i2 = b.i2; } else { o.m2 = a.m1; o.i2 = a.i1; }
+  }
+  return o;
+}
+
+// One wavefront per scored row: fold the per-vocab-tile partials (m1, i1, m2, i2, s) in a fixed
+// order (lane-strided, then a fixed butterfly), so the result is bitwise reproducible.
+// conf = 1 / S, p2 = exp(m2 - M) / S, lse = M + log S with M = global max, S = sum_t s_t e^(m1_t - M).
+__global__ void __launch_bounds__(256) merge_kernel(const float* __restrict__ pm1, const int32_t* __restrict__ pi1,
+                                                   const float* __restrict__ pm2, const int32_t* __restrict__ pi2,
+                                                   const float* __restrict__ ps, int n_vt,
+                                                   const int32_t* __restrict__ rows,
+                                                   const int32_t* __restrict__ count, dcl_row_stats st) {
+  int lane = threadIdx.x & 63;
+  int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= *count) return;
+  const size_t base = (size_t)j * n_vt;
+  Top2 t = {-INFINITY, -INFINITY, INT_MAX, INT_MAX};
+  for (int v = lane; v < n_vt; v += 64) {
+    Top2 x = {pm1[base + v], pm2[base + v], pi1[base + v], pi2[base + v]};
+    t = top2_merge(t, x);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    Top2 x = {__shfl_xor(t.m1, o, 64), __shfl_xor(t.m2, o, 64), __shfl_xor(t.i1, o, 64), __shfl_xor(t.i2, o, 64)};
+    // keep the operand order fixed (lower lane first) so every lane computes the same result
+    t = (lane & o) ? top2_merge(x, t) : top2_merge(t, x);
+  }
+  const float M = t.m1;
+  float s = 0.f;
+  for (int v = lane; v < n_vt; v += 64) s += ps[base + v] * __expf(pm1[base + v] - M);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) {
+    int row = rows[j];
+    st.top1[row] = t.i1;
+    st.top2[row] = t.i2;
+    st.conf[row] = 1.0f / s;
+    st.p2[row] = __expf(t.m2 - M) / s;
+    st.lse[row] = M + logf(s);
+  }
+}
+
+void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const int32_t* pi2, const float* ps,
+                  int n_vt, const int32_t* rows, const int32_t* count, int max_rows, dcl_row_stats st,
+                  hipStream_t s) {
+  if (max_rows == 0) return;
+  hipLaunchKernelGGL(merge_kernel, dim3((max_rows + 3) / 4), dim3(256), 0, s, pm1, pi1, pm2, pi2, ps, n_vt, rows,
+                     count, st);
+}
+
+// ---------------------------------------------------------------- DCV + drafts + remask
+// One workgroup per sequence.
+__global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ tokens, int S, int32_t* __restrict__ p,
+                                                    int gen_end, int L, float tau_c, float tau_d, int mask_id,
+                                                    dcl_row_stats st, int32_t* __restrict__ k_raw,
+                                                    int32_t* __restrict__ k_eff, uint32_t flags) {
+  __shared__ int red[4];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int32_t* x = tokens + (size_t)b * S;
+  const int32_t* top1 = st.top1 + (size_t)b * S;
+  const float* conf = st.conf + (size_t)b * S;
+  const int pb = p[b];
+  if (pb < 0 || pb >= gen_end) {  // finished (or invalid) pointer: the sequence is left untouched
+    if (tid == 0) {
+      if (k_raw) k_raw[b] = 0;
+      if (k_eff) k_eff[b] = 0;
+    }
+    return;
+  }
+  const int L_eff = min(L, gen_end - pb);
+  // window ends computed in 64-bit: p + L may exceed INT_MAX for a huge L
+  const int draft_start = (int)min((long)pb + L, (long)gen_end);
+  // K = index of the first window row that fails conf > tau_c (Eq. compute_k), L_eff if none.
+  int first = L_eff;
+  for (int j = tid; j < L_eff; j += 256)
+    if (!(conf[pb + j] > tau_c)) first = min(first, j);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
+  if (lane == 0) red[wid] = first;
+  __syncthreads();
+  const int K = min(min(red[0], red[1]), min(red[2], red[3]));
+  int Ke = K;
+  if (!(flags & DCL_SEL_NO_PROGRESS_GUARD) && Ke == 0 && top1[pb] >= 0) Ke = 1;
+  for (int j = tid; j < Ke; j += 256) x[pb + j] = top1[pb + j];
+  const bool any = (flags & DCL_SEL_SCORE_ALL) != 0;
+  for (int j = draft_start + tid; j < gen_end; j += 256)
+    if ((any || x[j] == mask_id) && conf[j] > tau_d && top1[j] >= 0) x[j] = top1[j];
+  __syncthreads();
+  const int pn = pb + Ke;
+  const int stop = (int)min((long)pn + L, (long)gen_end);
+  for (int j = pn + tid; j < stop; j += 256) x[j] = mask_id;
+  if (tid == 0) {
+    p[b] = pn;
+    if (k_raw) k_raw[b] = K;
+    if (k_eff) k_eff[b] = Ke;
+  }
+}
+
+void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c, float tau_d,
+                   int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff, uint32_t flags, hipStream_t s) {
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, tau_c, tau_d, mask_id, st,
+                     k_raw, k_eff, flags);
+}
+
+// ---------------------------------------------------------------- weight packing (load time)
+// Row permutations of the packed layout:
+//   mode 0: identity;
+//   mode 1: RoPE pair interleave within each head of `dh` rows: source row j (j < dh/2) -> 2j,
+//           source row j + dh/2 -> 2j + 1, so a rotation pair sits in adjacent rows;
+//   mode 2: gate row f -> 2f;  mode 3: up row f -> 2f + 1 (SwiGLU pairs adjacent).
+__device__ __forceinline__ int packed_row(int src, int mode, int dh) {
+  if (mode == 1) {
+    int h = src / dh, j = src % dh, half = dh / 2;
+    return h * dh + (j < half ? 2 * j : 2 * (j - half) + 1);
+  }
+  if (mode == 2) return 2 * src;
+  if (mode == 3) return 2 * src + 1;
+  return src;
+}
+
+__device__ __forceinline__ float load_src(const void* src, int dtype, size_t i) {
+  return dtype == DCL_DTYPE_F32 ? reinterpret_cast<const float*>(src)[i]
+                                : bf2f(reinterpret_cast<const bf16_t*>(src)[i]);
+}
+
+__global__ void pack_rows_kernel(const void* __restrict__ src, int dtype, bf16_t* __restrict__ dst, int rows,
+                                 int cols, int mode, int dh, int dst_row0) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t n = (size_t)rows * cols;
+  if (i >= n) return;
+  int r = (int)(i / cols), c = (int)(i % cols);
+  int pr = dst_row0 + packed_row(r, mode, dh);
+  dst[(size_t)pr * cols + c] = f2bf(load_src(src, dtype, i));
+}
+
+void launch_pack_rows(const void* src, int src_dtype, bf16_t* dst, int rows, int cols, int mode, int dh,
+                      int dst_row0, hipStream_t s) {
+  size_t n = (size_t)rows * cols;
+  if (n == 0) return;
+  hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, src_dtype, dst,
+                     rows, cols, mode, dh, dst_row0);
+}
+
+__global__ void pack_vec_kernel(const void* __restrict__ src, int dtype, float* __restrict__ dst, int n, int mode,
+                                int dh, int dst0) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  dst[dst0 + packed_row(i, mode, dh)] = src ? load_src(src, dtype, i) : 0.f;
+}
+
+void launch_pack_vec(const void* src, int src_dtype, float* dst, int n, int mode, int dh, int dst0,
+                     hipStream_t s) {
+  if (n == 0) return;
+  hipLaunchKernelGGL(pack_vec_kernel, dim3((n + 255) / 256), dim3(256), 0, s, src, src_dtype, dst, n, mode, dh,
+                     dst0);
+}
+
+}  // namespace dcl

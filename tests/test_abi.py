@@ -1,0 +1,110 @@
+"""CPU-only checks of the C ABI: the library loads, exports every symbol include/dcl.h declares,
+and rejects bad arguments on the host before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def dcl():
+    from paper_2607_20467_amd import build
+    if build.is_stale():
+        build.build()
+    import paper_2607_20467_amd as m
+    m.load_library()
+    return m
+
+
+def test_exports_every_declared_symbol(dcl):
+    header = open(os.path.join(ROOT, "include", "dcl.h")).read()
+    declared = set(re.findall(r"\b(dcl_[a-z_]+)\s*\(", header))
+    assert {"dcl_denoise_step", "dcl_select_contiguous", "dcl_load_weights"} <= declared
+    lib = ctypes.CDLL(dcl.library_path())
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(dcl):
+    assert dcl.dcl_status_string(0) == "ok"
+    assert "argument" in dcl.dcl_status_string(1)
+    assert dcl.dcl_status_string(99) == "unknown status"
+
+
+def _cfg(dcl, **kw):
+    c = dcl.config_from_geometry(synth.LLADA8B)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, 2), ("n_kv_heads", 5, 2), ("d_model", 4100, 2), ("d_ffn", 8, 2), ("vocab", 1, 1),
+    ("mask_id", 126464, 1), ("mask_id", -1, 1), ("rms_eps", 0.0, 1), ("rope_base", 1.0, 1),
+    ("max_positions", 0, 1), ("n_layers", 0, 1), ("qkv_bias", 2, 1)])
+def test_model_create_rejects(dcl, field, value, status):
+    with pytest.raises(dcl.DclError) as e:
+        dcl.dcl_model_create(_cfg(dcl, **{field: value}))
+    assert e.value.status == status
+    assert dcl.dcl_last_error()
+    assert dcl.dcl_weights_bytes(_cfg(dcl, **{field: value})) == 0
+
+
+def test_sizes(dcl):
+    cfg = _cfg(dcl)
+    wb = dcl.dcl_weights_bytes(cfg)
+    params = synth.LLADA8B.vocab * 4096 * 2 + 32 * (4 * 4096 * 4096 + 3 * 4096 * 12288)
+    assert params * 2 <= wb <= params * 2 + 64 * 2 ** 20        # bf16 matrices + small vectors / tables
+    m = dcl.dcl_model_create(cfg)
+    try:
+        a = dcl.dcl_workspace_bytes(m, 1, 384, 0)
+        assert a > 0 and dcl.dcl_workspace_bytes(m, 4, 768, 0) > a
+        assert dcl.dcl_workspace_bytes(m, 0, 384, 0) == 0
+        assert dcl.dcl_workspace_bytes(m, 1, 0, 0) == 0
+    finally:
+        dcl.dcl_model_destroy(m)
+
+
+def test_step_and_select_argument_checks_without_gpu(dcl):
+    """Every failure below is detected on the host; no HIP call is made (there is no GPU here)."""
+    lib = dcl.load_library()
+    m = dcl.dcl_model_create(_cfg(dcl))
+    try:
+        st = dcl.binding.DclRowStats(1, 1, 1, 1, 1)
+        # weights not loaded
+        r = lib.dcl_denoise_step(m, 8, 1, 384, 8, 384, None, 0, st, 256, 1 << 40, None)
+        assert r == 5 and "not loaded" in dcl.dcl_last_error()
+        # load: misaligned / too small / wrong count
+        arr = (ctypes.c_void_p * 3)(1, 2, 3)
+        assert lib.dcl_load_weights(m, 3, 1 << 40, arr, 3, 1, None) == 1
+        assert lib.dcl_load_weights(m, 256, 16, arr, 3, 1, None) == 3
+        assert lib.dcl_load_weights(m, 256, 1 << 40, arr, 3, 1, None) == 1
+        assert "n_src" in dcl.dcl_last_error()
+        assert lib.dcl_load_weights(m, 256, 1 << 40, arr, 3, 7, None) == 1
+    finally:
+        dcl.dcl_model_destroy(m)
+    sel = lib.dcl_select_contiguous
+    st = dcl.binding.DclRowStats(1, 1, 1, 1, 1)
+    assert sel(None, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 0, None) == 1
+    assert sel(8, 1, 8, 8, 9, 4, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # gen_end > S
+    assert sel(8, 1, 8, 8, 8, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # L = 0
+    assert sel(8, 1, 8, 8, 8, 4, 1.5, 0.98, 3, st, None, None, 0, None) == 1      # tau_commit > 1
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, -0.1, 3, st, None, None, 0, None) == 1      # tau_draft < 0
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 8, None) == 1      # unknown flag
+    assert "flags" in dcl.dcl_last_error()
+    bad = dcl.binding.DclRowStats(0, 1, 0, 1, 1)
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, bad, None, None, 0, None) == 1
+
+
+def test_product_has_no_oracle_dependency():
+    """The product package never imports the oracle (test infrastructure) or falls back to the CPU."""
+    pkg = os.path.join(ROOT, "paper_2607_20467_amd")
+    for fn in os.listdir(pkg):
+        if fn.endswith(".py"):
+            src = open(os.path.join(pkg, fn)).read()
+            assert not re.search(r"^\s*(import|from)\s+oracle", src, re.M), fn

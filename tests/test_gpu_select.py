@@ -1,0 +1,64 @@
+"""GPU parity of dcl_select_contiguous (DCV, commit, drafts, remask) against the oracle: bit-exact."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle.select import scored_mask
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0):
+    import torch
+    import paper_2607_20467_amd as dcl
+    B, S = tok.shape
+    t = torch.from_numpy(tok.astype(np.int32)).cuda()
+    pp = torch.from_numpy(p.astype(np.int32)).cuda()
+    st = {"top1": torch.from_numpy(top1.astype(np.int32)).cuda(),
+          "top2": torch.zeros((B, S), dtype=torch.int32, device="cuda"),
+          "conf": torch.from_numpy(conf.astype(np.float32)).cuda(),
+          "p2": torch.zeros((B, S), dtype=torch.float32, device="cuda"),
+          "lse": torch.zeros((B, S), dtype=torch.float32, device="cuda")}
+    kr = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    ke = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    dcl.dcl_select_contiguous(t, B, S, pp, end, L, tc, td, mask, st, kr, ke, flags)
+    torch.cuda.synchronize()
+    return t.cpu().numpy(), pp.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_select_random_states_bit_exact(seed):
+    rng = np.random.default_rng(100 + seed)
+    mask = 4095
+    B, S = int(rng.integers(1, 9)), int(rng.integers(8, 700))
+    end = int(rng.integers(1, S + 1))
+    L = int(rng.choice([1, 2, 16, 32, 64, 128, 300]))
+    tok = rng.integers(0, 4000, (B, S))
+    p = rng.integers(0, end + 1, B)
+    p[0] = min(p[0], end - 1)
+    for b in range(B):
+        tok[b, p[b]:] = np.where(rng.random(S - p[b]) < 0.6, mask, tok[b, p[b]:])
+        tok[b, p[b]:min(p[b] + L, end)] = mask                     # the window is masked before a step
+    for flags, score_all in ((0, False), (1, False), (2, True), (3, True)):
+        sc = scored_mask(tok, p, end, mask, score_all)
+        # float32 confidences, compared identically by both sides
+        conf = np.where(sc, rng.uniform(0, 1, (B, S)).astype(np.float32), np.float32(-1)).astype(np.float32)
+        conf[sc & (rng.random((B, S)) < 0.05)] = np.float32(0.7)   # exact ties with the threshold
+        top1 = np.where(sc, rng.integers(0, 4000, (B, S)), -1)
+        tc, td = np.float32(0.7), np.float32(rng.choice([0.5, 0.9, 0.98, 1.5]))
+        ref = oracle.select_contiguous(tok, p, end, L, float(tc), float(td), mask, top1, conf.astype(np.float64),
+                                       no_progress_guard=bool(flags & 1), score_all=score_all)
+        got = _run_gpu(tok, p, end, L, float(tc), float(td), mask, top1, conf, flags)
+        for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
+            np.testing.assert_array_equal(g, r, err_msg=f"{name} flags={flags} B={B} S={S} L={L} end={end}")
+
+
+def test_select_golden_cases():
+    import json
+    import os
+    cases = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "select_cases.json")))["select_cases"]
+    for c in cases:
+        got = _run_gpu(np.array([c["tokens"]]), np.array([c["p"]]), c["gen_end"], c["L"], c["tau_commit"],
+                       c["tau_draft"], c["mask_id"], np.array([c["top1"]]), np.array([c["conf"]], np.float32))
+        assert got[0][0].tolist() == c["expect_tokens"], c["name"]
+        assert (got[1][0], got[2][0], got[3][0]) == (c["expect_p"], c["expect_K_raw"], c["expect_K_eff"]), c["name"]
