@@ -154,11 +154,24 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
                                  dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,
                                  hipStream_t stream);
 
+/* Workspace bytes for dcl_score_hidden over n rows; 0 if the arguments are invalid. */
+size_t dcl_score_workspace_bytes(dcl_model_t model, int32_t n);
+
+/* The vocabulary reduction alone (the LM head and softmax statistics of Section 2.1, Eq. 2 and
+ * Eq. threshold_pd) on given final hidden states: hidden bf16 [n, d_model] (device, 16-byte
+ * aligned), already final-normalised. Writes statistics for rows 0..n-1 into `out` (each array
+ * has n entries). Logits are never written to memory. ws: device, 256-byte aligned,
+ * ws_bytes >= dcl_score_workspace_bytes(model, n). */
+dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dcl_row_stats out,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Test support: the same forward as dcl_denoise_step, then float32 logits of the rows listed in
- * `rows` (device [n_rows], flat indices b*S + i) into out (device [n_rows, vocab]). */
+ * `rows` (device [n_rows], flat indices b*S + i; an index outside [0, B*S) gives a zero hidden
+ * row) into out (device [n_rows, vocab]); if hidden_out is not NULL it also receives those rows'
+ * final hidden states (bf16 [n_rows, d_model]). */
 dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
                             const dcl_kv* kv, const int32_t* rows, int32_t n_rows, float* out,
-                            void* ws, size_t ws_bytes, hipStream_t stream);
+                            void* hidden_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -15,6 +15,10 @@ bfloat16 tensor, so both sides see the same operands:
   h_f = bf16(rmsnorm(r) * gf)
 Pure mode (``bf16_boundary=False``) drops those roundings (weights stay as given).
 The residual stream r is never rounded.
+
+``dtype=np.float32`` evaluates the same definition in float32 arithmetic. It is not the
+reference; it measures how far any float32 implementation of this rounding list lands from the
+float64 result, which sizes the whole-step tolerance of the GPU parity tests.
 """
 from typing import Callable, Mapping, Optional, Tuple
 
@@ -23,15 +27,15 @@ import numpy as np
 from .numerics import apply_rope, bf16_round, rmsnorm, rope_tables, silu
 
 
-def _w(weights, name) -> Optional[np.ndarray]:
+def _w(weights, name, dtype=np.float64) -> Optional[np.ndarray]:
     v = weights[name] if not callable(weights) else weights(name)
-    return None if v is None else np.asarray(v, dtype=np.float64)
+    return None if v is None else np.asarray(v, dtype=dtype)
 
 
 def forward(geom, weights, tokens: np.ndarray, positions: np.ndarray,
             kv: Optional[Callable[[int], Tuple[np.ndarray, np.ndarray]]] = None,
             bf16_boundary: bool = True, rope: bool = True, return_residuals: bool = False,
-            return_kv: bool = False):
+            return_kv: bool = False, dtype=np.float64):
     """Final hidden states h_f [S, d] (float64) of one sequence.
 
     geom: object with the geometry fields of ``synth.Geometry``.
@@ -43,25 +47,30 @@ def forward(geom, weights, tokens: np.ndarray, positions: np.ndarray,
     return_kv: also return the per-layer (k [Hkv,S,dh], v [Hkv,dh,S]) of the S tokens, as a cache would
         hold them.
     """
-    rnd = bf16_round if bf16_boundary else (lambda a: a)
+    dt = np.dtype(dtype)
+    if bf16_boundary:
+        rnd = lambda a: bf16_round(a).astype(dt)
+    else:
+        rnd = lambda a: a
     d, H, Hkv, dh = geom.d_model, geom.n_heads, geom.n_kv_heads, geom.head_dim
     S = len(tokens)
     group = H // Hkv
-    cos, sin = rope_tables(positions, dh, geom.rope_base)
+    cos, sin = (t.astype(dt) for t in rope_tables(positions, dh, geom.rope_base))
+    W = lambda name: _w(weights, name, dt)
 
-    r = _w(weights, "embed")[np.asarray(tokens)]                 # [S, d]
+    r = W("embed")[np.asarray(tokens)]                           # [S, d]
     residuals = [r.copy()] if return_residuals else None
     kv_out = [] if return_kv else None
     for l in range(geom.n_layers):
         p = f"l{l}."
-        u = rnd(rmsnorm(r, _w(weights, p + "g1"), geom.rms_eps))
-        q = u @ _w(weights, p + "wq").T
-        k = u @ _w(weights, p + "wk").T
-        v = u @ _w(weights, p + "wv").T
+        u = rnd(rmsnorm(r, W(p + "g1"), geom.rms_eps))
+        q = u @ W(p + "wq").T
+        k = u @ W(p + "wk").T
+        v = u @ W(p + "wv").T
         if geom.qkv_bias:
-            q = q + _w(weights, p + "bq")
-            k = k + _w(weights, p + "bk")
-            v = v + _w(weights, p + "bv")
+            q = q + W(p + "bq")
+            k = k + W(p + "bk")
+            v = v + W(p + "bv")
         q = q.reshape(S, H, dh).transpose(1, 0, 2)                # [H, S, dh]
         k = k.reshape(S, Hkv, dh).transpose(1, 0, 2)              # [Hkv, S, dh]
         v = v.reshape(S, Hkv, dh).transpose(1, 0, 2)
@@ -73,39 +82,40 @@ def forward(geom, weights, tokens: np.ndarray, positions: np.ndarray,
             kv_out.append((k.copy(), v.transpose(0, 2, 1).copy()))
         if kv is not None:
             kc, vc = kv(l)
-            k = np.concatenate([np.asarray(kc, np.float64), k], axis=1)
-            v = np.concatenate([np.asarray(vc, np.float64).transpose(0, 2, 1), v], axis=1)
-        o = np.empty((H, S, dh))
+            k = np.concatenate([np.asarray(kc, dt), k], axis=1)
+            v = np.concatenate([np.asarray(vc, dt).transpose(0, 2, 1), v], axis=1)
+        o = np.empty((H, S, dh), dt)
         for h in range(H):
             g = h // group
-            s = (q[h] @ k[g].T) / np.sqrt(dh)                      # [S, Sk], no mask
+            s = (q[h] @ k[g].T) / float(np.sqrt(dh))                     # [S, Sk], no mask
             s = np.exp(s - s.max(axis=1, keepdims=True))
             P = s / s.sum(axis=1, keepdims=True)
             o[h] = P @ v[g]
         o = rnd(o.transpose(1, 0, 2).reshape(S, H * dh))
-        r = r + o @ _w(weights, p + "wo").T
-        u2 = rnd(rmsnorm(r, _w(weights, p + "g2"), geom.rms_eps))
-        a = rnd(silu(u2 @ _w(weights, p + "wg").T) * (u2 @ _w(weights, p + "wu").T))
-        r = r + a @ _w(weights, p + "wd").T
+        r = r + o @ W(p + "wo").T
+        u2 = rnd(rmsnorm(r, W(p + "g2"), geom.rms_eps))
+        a = rnd(silu(u2 @ W(p + "wg").T) * (u2 @ W(p + "wu").T))
+        r = r + a @ W(p + "wd").T
         if return_residuals:
             residuals.append(r.copy())
-    hf = rnd(rmsnorm(r, _w(weights, "gf"), geom.rms_eps))
+    hf = rnd(rmsnorm(r, W("gf"), geom.rms_eps))
     extra = ([residuals] if return_residuals else []) + ([kv_out] if return_kv else [])
     return (hf, *extra) if extra else hf
 
 
-def lm_logits(weights, hf: np.ndarray, chunk: int = 8192) -> np.ndarray:
-    """logits = h_f W_lm^T in float64, never rounded; [R, V]. Vocabulary processed in chunks."""
+def lm_logits(weights, hf: np.ndarray, chunk: int = 8192, dtype=np.float64) -> np.ndarray:
+    """logits = h_f W_lm^T in float64 (or ``dtype``), never rounded; [R, V]. Vocabulary in chunks."""
     from .numerics import WeightView, weight_values
     if isinstance(weights, WeightView):
         raw = weights.stored["lm_head"]
-        get = lambda a, b: weight_values(raw[a:b], weights.bf16_boundary)
+        get = lambda a, b: weight_values(raw[a:b], weights.bf16_boundary).astype(dtype)
         V = raw.shape[0]
     else:
         W = weights["lm_head"] if not callable(weights) else weights("lm_head")
-        get = lambda a, b: np.asarray(W[a:b], np.float64)
+        get = lambda a, b: np.asarray(W[a:b], dtype)
         V = W.shape[0]
-    out = np.empty((hf.shape[0], V))
+    out = np.empty((hf.shape[0], V), dtype)
+    hf = np.asarray(hf, dtype)
     for v0 in range(0, V, chunk):
         out[:, v0:v0 + chunk] = hf @ get(v0, v0 + chunk).T
     return out

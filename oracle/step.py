@@ -12,13 +12,15 @@ from .select import scored_mask
 
 
 def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_boundary=True,
-         rope=True, return_logits_rows=None):
+         rope=True, return_logits_rows=None, dtype=np.float64, return_hidden=False):
     """Statistics dict with arrays [B, S]: top1, top2, conf, p2, lse.
 
     kv: optional callable (b, layer) -> (Kc [Hkv,P,dh], Vc [Hkv,dh,P]) with prefix length ``kv_prefix``
         given as attribute ``kv.prefix``; tokens are then at absolute positions prefix + i.
     return_logits_rows: optional list of flat row indices b*S+i whose float64 logits are also returned
         (key "logits", [len, V]); they need not be scored rows.
+    dtype: arithmetic of the evaluation (float64 = the oracle; float32 only sizes tolerances).
+    return_hidden: also return the final hidden states h_f [B, S, d] (key "hidden").
     """
     tokens = np.asarray(tokens)
     B, S = tokens.shape
@@ -32,28 +34,33 @@ def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_bound
     }
     want = {} if return_logits_rows is None else {int(r): n for n, r in enumerate(return_logits_rows)}
     logits_out = None if return_logits_rows is None else np.empty((len(want), geom.vocab))
+    hidden = np.zeros((B, S, geom.d_model)) if return_hidden else None
     prefix = 0 if kv is None else kv.prefix
     pos = prefix + np.arange(S)
     for b in range(B):
         extra = [i for i in range(S) if (b * S + i) in want]
         rows = np.nonzero(sc[b])[0]
-        if len(rows) == 0 and not extra:
+        if len(rows) == 0 and not extra and not return_hidden:
             continue
         kvb = None if kv is None else (lambda l, b=b: kv(b, l))
-        hf = forward(geom, weights, tokens[b], pos, kv=kvb, bf16_boundary=bf16_boundary, rope=rope)
+        hf = forward(geom, weights, tokens[b], pos, kv=kvb, bf16_boundary=bf16_boundary, rope=rope, dtype=dtype)
+        if return_hidden:
+            hidden[b] = hf
         if len(rows):
-            t1, t2, c, p2, lse = row_stats(lm_logits(weights, hf[rows]))
+            t1, t2, c, p2, lse = row_stats(lm_logits(weights, hf[rows], dtype=dtype))
             out["top1"][b, rows] = t1
             out["top2"][b, rows] = t2
             out["conf"][b, rows] = c
             out["p2"][b, rows] = p2
             out["lse"][b, rows] = lse
         if extra:
-            lg = lm_logits(weights, hf[extra])
+            lg = lm_logits(weights, hf[extra], dtype=dtype)
             for n, i in enumerate(extra):
                 logits_out[want[b * S + i]] = lg[n]
     if logits_out is not None:
         out["logits"] = logits_out
+    if return_hidden:
+        out["hidden"] = hidden
     return out
 
 

@@ -69,7 +69,9 @@ def load_library():
                                             vp, sz, vp]),
         "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, f32, f32, i32, DclRowStats, vp, vp,
                                                  u32, vp]),
-        "dcl_debug_logits": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, i32, vp, vp, sz, vp]),
+        "dcl_score_workspace_bytes": (sz, [vp, i32]),
+        "dcl_score_hidden": (ctypes.c_int, [vp, vp, i32, DclRowStats, vp, sz, vp]),
+        "dcl_debug_logits": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, i32, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -164,11 +166,20 @@ def dcl_select_contiguous(tokens, B: int, S: int, p, gen_end: int, L: int, tau_c
                                                 _stream(stream)), "dcl_select_contiguous")
 
 
-def dcl_debug_logits(model: int, tokens, B: int, S: int, kv, rows, n_rows: int, out, ws, ws_bytes: int,
+def dcl_score_workspace_bytes(model: int, n: int) -> int:
+    return load_library().dcl_score_workspace_bytes(model, n)
+
+
+def dcl_score_hidden(model: int, hidden, n: int, stats, ws, ws_bytes: int, stream=None) -> None:
+    _check(load_library().dcl_score_hidden(model, _ptr(hidden), n, _stats(stats), _ptr(ws), ws_bytes,
+                                           _stream(stream)), "dcl_score_hidden")
+
+
+def dcl_debug_logits(model: int, tokens, B: int, S: int, kv, rows, n_rows: int, out, hidden_out, ws, ws_bytes: int,
                      stream=None) -> None:
     kvp, keep = _kv(kv)
-    _check(load_library().dcl_debug_logits(model, _ptr(tokens), B, S, kvp, _ptr(rows), n_rows, _ptr(out), _ptr(ws),
-                                           ws_bytes, _stream(stream)), "dcl_debug_logits")
+    _check(load_library().dcl_debug_logits(model, _ptr(tokens), B, S, kvp, _ptr(rows), n_rows, _ptr(out),
+                                           _ptr(hidden_out), _ptr(ws), ws_bytes, _stream(stream)), "dcl_debug_logits")
     del keep
 
 
@@ -239,12 +250,24 @@ class Runner:
         dcl_denoise_step(self.model, tokens, B, S, p, gen_end, kv, flags, stats, ws, n, stream)
         return stats
 
-    def logits(self, tokens, rows, kv=None, stream=None):
+    def logits(self, tokens, rows, kv=None, stream=None, with_hidden=False):
+        """float32 logits [n_rows, V] (and, with_hidden, bf16-bit hidden states [n_rows, d] as int16)."""
         B, S = tokens.shape
         ws, n = self.workspace(B, S, 0 if kv is None else kv[2])
         out = self.torch.empty((rows.numel(), self.geom.vocab), dtype=self.torch.float32, device="cuda")
-        dcl_debug_logits(self.model, tokens, B, S, kv, rows, rows.numel(), out, ws, n, stream)
-        return out
+        hid = self.torch.empty((rows.numel(), self.geom.d_model), dtype=self.torch.int16, device="cuda") \
+            if with_hidden else None
+        dcl_debug_logits(self.model, tokens, B, S, kv, rows, rows.numel(), out, hid, ws, n, stream)
+        return (out, hid) if with_hidden else out
+
+    def score_hidden(self, hidden, stream=None):
+        """Statistics of given bf16 hidden rows (int16 bit patterns or torch.bfloat16, [n, d])."""
+        n = hidden.shape[0]
+        need = dcl_score_workspace_bytes(self.model, n)
+        ws = self.torch.empty(need, dtype=self.torch.uint8, device="cuda")
+        st = self.new_stats(1, n)
+        dcl_score_hidden(self.model, hidden, n, st, ws, need, stream)
+        return {k: v.view(n) for k, v in st.items()}
 
     def close(self):
         if self.model:

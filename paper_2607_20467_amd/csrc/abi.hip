@@ -374,9 +374,72 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
   return hip_check(hipGetLastError(), "select launch");
 }
 
+struct ScoreLayout {
+  size_t rows, count, pm1, pi1, pm2, pi2, ps, total;
+  int n_vt;
+};
+
+static ScoreLayout score_layout(const dcl_config& c, int n) {
+  ScoreLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  L.n_vt = (c.vocab + kLmTile - 1) / kLmTile;
+  L.rows = take((size_t)n * 4);
+  L.count = take(4);
+  const size_t np = (size_t)n * L.n_vt * 4;
+  L.pm1 = take(np);
+  L.pi1 = take(np);
+  L.pm2 = take(np);
+  L.pi2 = take(np);
+  L.ps = take(np);
+  L.total = off;
+  return L;
+}
+
+size_t dcl_score_workspace_bytes(dcl_model_t model, int32_t n) {
+  Model* m = reinterpret_cast<Model*>(model);
+  if (!m || n < 1 || n > (1 << 22)) return 0;
+  return score_layout(m->cfg, n).total;
+}
+
+dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dcl_row_stats out, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  if (!m) return fail(DCL_E_ARG, "model is NULL");
+  if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
+  if (!hidden) return fail(DCL_E_ARG, "hidden is NULL");
+  if ((reinterpret_cast<uintptr_t>(hidden) & 15) != 0) return fail(DCL_E_ARG, "hidden must be 16-byte aligned");
+  if (n < 1 || n > (1 << 22)) return fail(DCL_E_ARG, "n=%d outside [1, 2^22]", n);
+  if (!out.top1 || !out.top2 || !out.conf || !out.p2 || !out.lse) return fail(DCL_E_ARG, "an output array is NULL");
+  if (!ws) return fail(DCL_E_ARG, "workspace is NULL");
+  if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(DCL_E_ARG, "workspace must be 256-byte aligned");
+  const ScoreLayout L = score_layout(m->cfg, n);
+  if (ws_bytes < L.total) return fail(DCL_E_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, L.total);
+  (void)hipGetLastError();
+  int32_t* rows = at<int32_t>(ws, L.rows);
+  int32_t* count = at<int32_t>(ws, L.count);
+  launch_iota(rows, count, n, stream);
+  LmOut lo;
+  lo.pm1 = at<float>(ws, L.pm1);
+  lo.pi1 = at<int32_t>(ws, L.pi1);
+  lo.pm2 = at<float>(ws, L.pm2);
+  lo.pi2 = at<int32_t>(ws, L.pi2);
+  lo.ps = at<float>(ws, L.ps);
+  lo.n_vt = L.n_vt;
+  lo.count = count;
+  gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), static_cast<const bf16_t*>(hidden), m->cfg.vocab, n, m->cfg.d_model, lo,
+              stream);
+  launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, n, out, stream);
+  return hip_check(hipGetLastError(), "score_hidden launch");
+}
+
 dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv,
-                            const int32_t* rows, int32_t n_rows, float* out, void* ws, size_t ws_bytes,
-                            hipStream_t stream) {
+                            const int32_t* rows, int32_t n_rows, float* out, void* hidden_out, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
   Model* m = reinterpret_cast<Model*>(model);
   dcl_status st = check_step_args(m, tokens, B, S, kv, ws, ws_bytes);
   if (st != DCL_OK) return st;
@@ -386,15 +449,17 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
   const StepLayout L = step_layout(c, B, S);
   (void)hipGetLastError();
   run_forward(m, tokens, B, S, kv, ws, L, stream);
+  // the row count goes to the device through a kernel argument (no host buffer to keep alive)
   int32_t* count = at<int32_t>(ws, L.count);
-  st = hip_check(hipMemcpyAsync(count, &n_rows, 4, hipMemcpyHostToDevice, stream), "hipMemcpyAsync(count)");
-  if (st != DCL_OK) return st;
-  // the host value must stay alive until the copy ran
-  st = hip_check(hipStreamSynchronize(stream), "hipStreamSynchronize(debug)");
-  if (st != DCL_OK) return st;
+  launch_iota(at<int32_t>(ws, L.pm1), count, n_rows, stream);
   bf16_t* hf = at<bf16_t>(ws, L.hf);
   launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count, stream);
   gemm_store_f32(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, n_rows, c.d_model, out, stream);
+  if (hidden_out) {
+    st = hip_check(hipMemcpyAsync(hidden_out, hf, (size_t)n_rows * c.d_model * 2, hipMemcpyDeviceToDevice, stream),
+                   "hipMemcpyAsync(hidden_out)");
+    if (st != DCL_OK) return st;
+  }
   return hip_check(hipGetLastError(), "debug_logits launch");
 }
 

@@ -56,6 +56,7 @@ void launch_compact(const int32_t* tokens, const int32_t* p, int B, int S, int g
 void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const int32_t* pi2,
                   const float* ps, int n_vt, const int32_t* rows, const int32_t* count, int max_rows,
                   dcl_row_stats st, hipStream_t s);
+void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s);
 void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c,
                    float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
                    uint32_t flags, hipStream_t s);

@@ -203,6 +203,17 @@ void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const 
                      count, st);
 }
 
+// rows[j] = j for j < n, count = n (row map of dcl_score_hidden and dcl_debug_logits' copy).
+__global__ void iota_kernel(int32_t* __restrict__ rows, int32_t* __restrict__ count, int n) {
+  int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j < n) rows[j] = j;
+  if (j == 0) *count = n;
+}
+
+void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s) {
+  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, rows, count, n);
+}
+
 // ---------------------------------------------------------------- DCV + drafts + remask
 // One workgroup per sequence.
 __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ tokens, int S, int32_t* __restrict__ p,
