@@ -1,0 +1,206 @@
+"""Throughput of one DC-Leap denoising iteration on one MI355X.
+
+A step = dcl_denoise_step (bidirectional transformer forward, fused LM head + vocabulary softmax /
+top-2 reduction over the masked rows) + dcl_select_contiguous (DCV, commit, drafts, remask), on
+one HIP stream, preceded by a device-to-device restore of the frozen decode state (tokens + p,
+1.5 KB) so every timed step sees the same input. Weights and inputs are seeded synthetic data
+resident in HBM before timing starts.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import dataclasses
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "denoising steps/sec and scored tokens/sec at LLaDA-8B shape; MFMA util %"
+BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def step_work(w, R):
+    """Algorithmic FLOPs per launch of each kernel class for workload w with R scored rows."""
+    g = w.geom
+    T = w.batch * w.seq
+    Sk = w.kv_prefix + w.seq
+    d, H, Hkv, dh, F, V = g.d_model, g.n_heads, g.n_kv_heads, g.head_dim, g.d_ffn, g.vocab
+    return {
+        "gemm_qkv_rope": 2.0 * T * (H + 2 * Hkv) * dh * d,
+        "attention": 4.0 * w.batch * H * w.seq * Sk * dh,
+        "gemm_o_residual": 2.0 * T * d * H * dh,
+        "gemm_gate_up_swiglu": 2.0 * T * 2 * F * d,
+        "gemm_down_residual": 2.0 * T * d * F,
+        "gemm_lm_head_top2": 2.0 * R * V * d,
+    }
+
+
+def step_flops(w, R):
+    per = step_work(w, R)
+    L = w.geom.n_layers
+    return L * sum(v for k, v in per.items() if k != "gemm_lm_head_top2") + per["gemm_lm_head_top2"]
+
+
+def cpu_baseline(w, stored, tok, p, R, layers_sample=8, rows_sample=64):
+    """The float64 oracle on a bounded sample of the same step, scaled to one full step."""
+    import numpy as np
+    import oracle
+    from oracle.numerics import WeightView
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    W = WeightView(stored)
+    g = w.geom
+    gs = dataclasses.replace(g, n_layers=layers_sample)
+    pos = np.arange(w.seq)
+    t0 = time.perf_counter()
+    hf = oracle.forward(gs, W, tok[0], pos)
+    t1 = time.perf_counter()
+    rows = np.nonzero(oracle.scored_mask(tok, p, w.gen_end, g.mask_id)[0])[0][:rows_sample]
+    oracle.row_stats(oracle.lm_logits(W, hf[rows]))
+    t2 = time.perf_counter()
+    est = (t1 - t0) * g.n_layers / layers_sample + (t2 - t1) * R / len(rows)
+    return {"value": 1.0 / est, "unit": "steps/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"float64 oracle forward over {layers_sample} of {g.n_layers} layers ({t1 - t0:.1f} s) and "
+                      f"LM head + softmax statistics for {len(rows)} of {R} scored rows ({t2 - t1:.1f} s), "
+                      f"scaled to one full step: {est:.1f} s/step",
+            "seconds_per_step": est}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c2", help="synth workload key (c2 = LLaDA-8B shape, B1, S384)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip the event-timed kernel-class pass")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
+              "one process drives one GPU", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_20467_amd as dcl
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    g = w.geom
+    log(f"workload {w.key}: {w.description}")
+    t = time.perf_counter()
+    stored = synth.make_weights(g)
+    log(f"generated {g.name} weights in {time.perf_counter() - t:.1f} s")
+    names = [n for n, _, _ in synth.tensor_specs(g)]
+    t = time.perf_counter()
+    run = dcl.Runner(g, [stored[n] for n in names], max_positions=max(4096, w.kv_prefix + w.seq))
+    log(f"loaded weights into HBM in {time.perf_counter() - t:.1f} s")
+    tok_h, p_h = synth.initial_state(w)
+    B, S = tok_h.shape
+    R = int(((tok_h == g.mask_id) & (np.arange(S)[None] >= p_h[:, None]) & (np.arange(S)[None] < w.gen_end)).sum())
+    tok0 = torch.from_numpy(tok_h).cuda()
+    p0 = torch.from_numpy(p_h).cuda()
+    tok = tok0.clone()
+    p = p0.clone()
+    kv = None
+    if w.kv_prefix:
+        caches = [synth.kv_cache_layer(w, l) for l in range(g.n_layers)]
+        kv = ([torch.from_numpy(c[0].view(np.int16)).cuda() for c in caches],
+              [torch.from_numpy(c[1].view(np.int16)).cuda() for c in caches], w.kv_prefix)
+        del caches
+    stats = run.new_stats(B, S)
+    ws, ws_bytes = run.workspace(B, S, w.kv_prefix)
+    k_raw = torch.zeros(B, dtype=torch.int32, device="cuda")
+    k_eff = torch.zeros(B, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def one_step():
+        tok.copy_(tok0, non_blocking=True)
+        p.copy_(p0, non_blocking=True)
+        dcl.dcl_denoise_step(run.model, tok, B, S, p, w.gen_end, kv, 0, stats, ws, ws_bytes, stream)
+        dcl.dcl_select_contiguous(tok, B, S, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id, stats,
+                                  k_raw, k_eff, 0, stream)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        one_step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = 1000.0 * elapsed / args.steps
+    steps_per_s = 1000.0 / ms
+    flops = step_flops(w, R)
+    mfma_util = 100.0 * flops / (ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12)
+    log(f"{ms:.3f} ms/step, {steps_per_s:.1f} steps/s, {R * steps_per_s:.0f} scored tok/s, "
+        f"{flops / 1e12:.3f} TFLOP/step -> {mfma_util:.1f}% of bf16 peak; K_eff {k_eff.cpu().tolist()}")
+
+    roofline = None
+    classes = None
+    if not args.no_profile:
+        dcl.dcl_profile_enable(True)
+        for _ in range(args.steps):
+            one_step()
+        torch.cuda.synchronize()
+        prof = dcl.dcl_profile_read()
+        dcl.dcl_profile_enable(False)
+        per = step_work(w, R)
+        classes = {}
+        for name, (n, tms) in prof.items():
+            if n == 0:
+                continue
+            avg_us = 1000.0 * tms / n
+            ent = {"launches_per_step": n / args.steps, "avg_us": round(avg_us, 2),
+                   "ms_per_step": round(tms / args.steps, 4)}
+            if name in per:
+                ent["tflops"] = round(per[name] / (avg_us * 1e-6) / 1e12, 1)
+            classes[name] = ent
+            log(f"  {name:22s} {n / args.steps:6.1f} launches/step  avg {avg_us:9.2f} us  "
+                f"{tms / args.steps:8.3f} ms/step" + (f"  {ent['tflops']:7.1f} TFLOP/s" if "tflops" in ent else ""))
+        dom = max((k for k in classes if k in per), key=lambda k: classes[k]["ms_per_step"])
+        ach = per[dom] / (classes[dom]["avg_us"] * 1e-6) / 1e12
+        roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                    "flop_per_launch": per[dom]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle on a bounded sample (CPU baseline)")
+        cpu = cpu_baseline(w, stored, tok_h, p_h, R)
+        cpu = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cpu.items()}
+        log(f"  {cpu['sample']}")
+
+    out = {
+        "metric": METRIC, "value": round(steps_per_s, 3), "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.key}: {w.description}", "geometry": g.name, "batch": B, "seq_len": S,
+                   "kv_prefix": w.kv_prefix, "scored_rows": R, "window": w.window, "tau_commit": w.tau_commit,
+                   "tau_draft": w.tau_draft, "parallelism": "single GPU"},
+        "scored_tokens_per_s": round(R * steps_per_s, 1),
+        "mfma_util_pct": round(mfma_util, 2),
+        "tflop_per_step": round(flops / 1e12, 4),
+        "roofline": roofline,
+        "kernel_classes": classes,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -173,6 +173,25 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
                             const dcl_kv* kv, const int32_t* rows, int32_t n_rows, float* out,
                             void* hidden_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Kernel-class timing (profiling support for benchmarks). While enabled, every kernel launch
+ * made by dcl_denoise_step / dcl_score_hidden / dcl_select_contiguous is bracketed by a pair of
+ * hipEvents recorded on the caller's stream (this adds a little host work per launch; leave it
+ * off for throughput runs). dcl_profile_read synchronises the recorded events and returns, per
+ * kernel class, the number of launches and the summed GPU time between each pair. Classes:
+ * 0 embed, 1 rmsnorm, 2 gemm_qkv_rope, 3 attention, 4 gemm_o_residual, 5 gemm_gate_up_swiglu,
+ * 6 gemm_down_residual, 7 compact_rows, 8 gemm_lm_head_top2, 9 merge_partials, 10 select.
+ * Host-side state, per process; not thread-safe. */
+enum { DCL_PROF_CLASSES = 11 };
+typedef struct {
+  int64_t launches[DCL_PROF_CLASSES];
+  double ms[DCL_PROF_CLASSES];
+} dcl_profile;
+
+/* on = 1 starts recording (and clears previous totals), on = 0 stops. */
+dcl_status dcl_profile_enable(int32_t on);
+/* Totals since the last enable (host struct). Blocks until every recorded event has completed. */
+dcl_status dcl_profile_read(dcl_profile* out);
+
 #ifdef __cplusplus
 }
 #endif

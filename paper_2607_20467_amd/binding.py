@@ -35,6 +35,14 @@ class DclRowStats(ctypes.Structure):
                 ("p2", ctypes.c_void_p), ("lse", ctypes.c_void_p)]
 
 
+PROF_CLASSES = ("embed", "rmsnorm", "gemm_qkv_rope", "attention", "gemm_o_residual", "gemm_gate_up_swiglu",
+                "gemm_down_residual", "compact_rows", "gemm_lm_head_top2", "merge_partials", "select")
+
+
+class DclProfile(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64 * len(PROF_CLASSES)), ("ms", ctypes.c_double * len(PROF_CLASSES))]
+
+
 class DclKV(ctypes.Structure):
     _fields_ = [("k", ctypes.POINTER(ctypes.c_void_p)), ("v", ctypes.POINTER(ctypes.c_void_p)),
                 ("prefix_len", ctypes.c_int32)]
@@ -70,6 +78,8 @@ def load_library():
         "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, f32, f32, i32, DclRowStats, vp, vp,
                                                  u32, vp]),
         "dcl_score_workspace_bytes": (sz, [vp, i32]),
+        "dcl_profile_enable": (ctypes.c_int, [i32]),
+        "dcl_profile_read": (ctypes.c_int, [ctypes.POINTER(DclProfile)]),
         "dcl_score_hidden": (ctypes.c_int, [vp, vp, i32, DclRowStats, vp, sz, vp]),
         "dcl_debug_logits": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, i32, vp, vp, vp, sz, vp]),
     }
@@ -164,6 +174,17 @@ def dcl_select_contiguous(tokens, B: int, S: int, p, gen_end: int, L: int, tau_c
     _check(load_library().dcl_select_contiguous(_ptr(tokens), B, S, _ptr(p), gen_end, L, tau_commit, tau_draft,
                                                 mask_id, _stats(stats), _ptr(k_raw), _ptr(k_eff), flags,
                                                 _stream(stream)), "dcl_select_contiguous")
+
+
+def dcl_profile_enable(on: bool) -> None:
+    _check(load_library().dcl_profile_enable(1 if on else 0), "dcl_profile_enable")
+
+
+def dcl_profile_read() -> dict:
+    """{class name: (launches, total ms)} since the last enable."""
+    pr = DclProfile()
+    _check(load_library().dcl_profile_read(ctypes.byref(pr)), "dcl_profile_read")
+    return {n: (int(pr.launches[i]), float(pr.ms[i])) for i, n in enumerate(PROF_CLASSES)}
 
 
 def dcl_score_workspace_bytes(model: int, n: int) -> int:

@@ -119,6 +119,65 @@ T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off);
 }
 
+// ---------------------------------------------------------------- kernel-class timing
+struct Profiler {
+  bool on = false;
+  struct Rec {
+    int cls;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  int64_t launches[DCL_PROF_CLASSES] = {};
+  double ms[DCL_PROF_CLASSES] = {};
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  // fold completed records into the totals once many are pending (bounds the event count)
+  void drain(bool wait) {
+    for (Rec& r : recs) {
+      if (wait) (void)hipEventSynchronize(r.b);
+      float t = 0.f;
+      if (hipEventElapsedTime(&t, r.a, r.b) == hipSuccess) {
+        ms[r.cls] += t;
+        launches[r.cls] += 1;
+      }
+      pool.push_back(r.a);
+      pool.push_back(r.b);
+    }
+    recs.clear();
+  }
+};
+Profiler g_prof;
+
+struct ProfScope {
+  hipStream_t s;
+  int cls;
+  hipEvent_t a = nullptr;
+  ProfScope(int c, hipStream_t st) : s(st), cls(c) {
+    if (!g_prof.on) return;
+    if (g_prof.recs.size() > 8192) g_prof.drain(true);
+    a = g_prof.get();
+    if (a) (void)hipEventRecord(a, s);
+  }
+  ~ProfScope() {
+    if (!a) return;
+    hipEvent_t b = g_prof.get();
+    if (!b) return;
+    (void)hipEventRecord(b, s);
+    g_prof.recs.push_back({cls, a, b});
+  }
+};
+enum { P_EMBED, P_NORM, P_QKV, P_ATTN, P_O, P_GU, P_DOWN, P_COMPACT, P_LM, P_MERGE, P_SELECT };
+#define PROF(cls) ProfScope prof_scope_##__LINE__(cls, s)
+
 dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv, void* ws,
                            size_t ws_bytes) {
   if (!m) return fail(DCL_E_ARG, "model is NULL");
@@ -153,10 +212,16 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
   bf16_t* u = at<bf16_t>(ws, L.u);
   bf16_t* a = at<bf16_t>(ws, L.a);
   bf16_t* o = at<bf16_t>(ws, L.o);
-  launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, s);
+  {
+    PROF(P_EMBED);
+    launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, s);
+  }
   for (int l = 0; l < c.n_layers; ++l) {
     const LayerOffsets& lo = m->lay.layer[l];
-    launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, s);
+    {
+      PROF(P_NORM);
+      launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, s);
+    }
     QkvOut qo;
     qo.q = at<bf16_t>(ws, L.q);
     qo.k = at<bf16_t>(ws, L.k);
@@ -169,7 +234,10 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     qo.S = S;
     qo.Sp = L.Sp;
     qo.pos0 = P;
-    gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
+    {
+      PROF(P_QKV);
+      gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
+    }
     AttnArgs aa;
     aa.q = qo.q;
     aa.k = qo.k;
@@ -185,11 +253,26 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     aa.Sp = L.Sp;
     aa.P = P;
     aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
-    launch_attention(aa, s);
-    gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, s);
-    launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, s);
-    gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
-    gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, s);
+    {
+      PROF(P_ATTN);
+      launch_attention(aa, s);
+    }
+    {
+      PROF(P_O);
+      gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, s);
+    }
+    {
+      PROF(P_NORM);
+      launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, s);
+    }
+    {
+      PROF(P_GU);
+      gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
+    }
+    {
+      PROF(P_DOWN);
+      gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, s);
+    }
   }
 }
 
@@ -341,10 +424,18 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   run_forward(m, tokens, B, S, kv, ws, L, stream);
   int32_t* rows = at<int32_t>(ws, L.rows);
   int32_t* count = at<int32_t>(ws, L.count);
-  launch_compact(tokens, p, B, S, gen_end, c.mask_id, (flags & DCL_SCORE_ALL_UNCOMMITTED) ? 1 : 0, rows, count, out,
-                 stream);
+  hipStream_t s = stream;
+  {
+    PROF(P_COMPACT);
+    launch_compact(tokens, p, B, S, gen_end, c.mask_id, (flags & DCL_SCORE_ALL_UNCOMMITTED) ? 1 : 0, rows, count, out,
+                   stream);
+  }
   bf16_t* hf = at<bf16_t>(ws, L.hf);
-  launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count, stream);
+  {
+    PROF(P_NORM);
+    launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count,
+                   stream);
+  }
   LmOut lo;
   lo.pm1 = at<float>(ws, L.pm1);
   lo.pi1 = at<int32_t>(ws, L.pi1);
@@ -353,8 +444,14 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   lo.ps = at<float>(ws, L.ps);
   lo.n_vt = L.n_vt;
   lo.count = count;
-  gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
-  launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, L.T, out, stream);
+  {
+    PROF(P_LM);
+    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
+  }
+  {
+    PROF(P_MERGE);
+    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, L.T, out, stream);
+  }
   return hip_check(hipGetLastError(), "denoise_step launch");
 }
 
@@ -370,7 +467,11 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
   if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
   if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL)) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
   (void)hipGetLastError();
-  launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, in, K_raw, K_eff, flags, stream);
+  {
+    hipStream_t s = stream;
+    PROF(P_SELECT);
+    launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, in, K_raw, K_eff, flags, stream);
+  }
   return hip_check(hipGetLastError(), "select launch");
 }
 
@@ -422,6 +523,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   (void)hipGetLastError();
   int32_t* rows = at<int32_t>(ws, L.rows);
   int32_t* count = at<int32_t>(ws, L.count);
+  hipStream_t s = stream;
   launch_iota(rows, count, n, stream);
   LmOut lo;
   lo.pm1 = at<float>(ws, L.pm1);
@@ -431,9 +533,15 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   lo.ps = at<float>(ws, L.ps);
   lo.n_vt = L.n_vt;
   lo.count = count;
-  gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), static_cast<const bf16_t*>(hidden), m->cfg.vocab, n, m->cfg.d_model, lo,
-              stream);
-  launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, n, out, stream);
+  {
+    PROF(P_LM);
+    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), static_cast<const bf16_t*>(hidden), m->cfg.vocab, n, m->cfg.d_model,
+                lo, stream);
+  }
+  {
+    PROF(P_MERGE);
+    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, n, out, stream);
+  }
   return hip_check(hipGetLastError(), "score_hidden launch");
 }
 
@@ -461,6 +569,29 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
     if (st != DCL_OK) return st;
   }
   return hip_check(hipGetLastError(), "debug_logits launch");
+}
+
+dcl_status dcl_profile_enable(int32_t on) {
+  if (on != 0 && on != 1) return fail(DCL_E_ARG, "on must be 0 or 1");
+  if (on) {
+    g_prof.drain(true);
+    for (int i = 0; i < DCL_PROF_CLASSES; ++i) {
+      g_prof.launches[i] = 0;
+      g_prof.ms[i] = 0.0;
+    }
+  }
+  g_prof.on = on != 0;
+  return DCL_OK;
+}
+
+dcl_status dcl_profile_read(dcl_profile* out) {
+  if (!out) return fail(DCL_E_ARG, "out is NULL");
+  g_prof.drain(true);
+  for (int i = 0; i < DCL_PROF_CLASSES; ++i) {
+    out->launches[i] = g_prof.launches[i];
+    out->ms[i] = g_prof.ms[i];
+  }
+  return DCL_OK;
 }
 
 }  // extern "C"
