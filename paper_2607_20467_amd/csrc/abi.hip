@@ -110,6 +110,19 @@ StepLayout step_layout(const dcl_config& c, int B, int S) {
   L.pm2 = take(np);
   L.pi2 = take(np);
   L.ps = take(np);
+  // split-K scratch of the four per-layer GEMMs (their shapes are fixed by B*S)
+  const int Ti = (int)T, qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const GemmPlan plans[4] = {plan_gemm(qkv, Ti, c.d_model, 0, 4), plan_gemm(c.d_model, Ti, c.n_heads * c.head_dim, 0, 4),
+                             plan_gemm(2 * c.d_ffn, Ti, c.d_model, 0, 4), plan_gemm(c.d_model, Ti, c.d_ffn, 0, 4)};
+  size_t part = 0;
+  int ntile = 1;
+  for (const GemmPlan& gp : plans) {
+    if (gemm_partial_bytes(gp) > part) part = gemm_partial_bytes(gp);
+    if (gp.nsplit > 1 && gp.tiles > ntile) ntile = gp.tiles;
+  }
+  L.gpart = take(part ? part : 16);
+  L.gcnt = take((size_t)ntile * 4);
+  L.n_cnt = ntile;
   L.total = off;
   return L;
 }
@@ -212,9 +225,10 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
   bf16_t* u = at<bf16_t>(ws, L.u);
   bf16_t* a = at<bf16_t>(ws, L.a);
   bf16_t* o = at<bf16_t>(ws, L.o);
+  const GemmScratch sc{at<float>(ws, L.gpart), at<int32_t>(ws, L.gcnt)};
   {
     PROF(P_EMBED);
-    launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, s);
+    launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, at<int32_t>(ws, L.gcnt), L.n_cnt, s);
   }
   for (int l = 0; l < c.n_layers; ++l) {
     const LayerOffsets& lo = m->lay.layer[l];
@@ -236,7 +250,7 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     qo.pos0 = P;
     {
       PROF(P_QKV);
-      gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
+      gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, sc, s);
     }
     AttnArgs aa;
     aa.q = qo.q;
@@ -259,7 +273,7 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     }
     {
       PROF(P_O);
-      gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, s);
+      gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, sc, s);
     }
     {
       PROF(P_NORM);
@@ -267,11 +281,11 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     }
     {
       PROF(P_GU);
-      gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
+      gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, sc, s);
     }
     {
       PROF(P_DOWN);
-      gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, s);
+      gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, sc, s);
     }
   }
 }
@@ -446,7 +460,8 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   lo.count = count;
   {
     PROF(P_LM);
-    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
+    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, GemmScratch{nullptr, nullptr},
+                stream);
   }
   {
     PROF(P_MERGE);
@@ -524,7 +539,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   int32_t* rows = at<int32_t>(ws, L.rows);
   int32_t* count = at<int32_t>(ws, L.count);
   hipStream_t s = stream;
-  launch_iota(rows, count, n, stream);
+  launch_iota(rows, count, n, nullptr, 0, stream);
   LmOut lo;
   lo.pm1 = at<float>(ws, L.pm1);
   lo.pi1 = at<int32_t>(ws, L.pi1);
@@ -536,7 +551,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   {
     PROF(P_LM);
     gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), static_cast<const bf16_t*>(hidden), m->cfg.vocab, n, m->cfg.d_model,
-                lo, stream);
+                lo, GemmScratch{nullptr, nullptr}, stream);
   }
   {
     PROF(P_MERGE);
@@ -559,10 +574,11 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
   run_forward(m, tokens, B, S, kv, ws, L, stream);
   // the row count goes to the device through a kernel argument (no host buffer to keep alive)
   int32_t* count = at<int32_t>(ws, L.count);
-  launch_iota(at<int32_t>(ws, L.pm1), count, n_rows, stream);
+  launch_iota(at<int32_t>(ws, L.pm1), count, n_rows, nullptr, 0, stream);
   bf16_t* hf = at<bf16_t>(ws, L.hf);
   launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count, stream);
-  gemm_store_f32(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, n_rows, c.d_model, out, stream);
+  gemm_store_f32(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, n_rows, c.d_model, out, GemmScratch{nullptr, nullptr},
+                 stream);
   if (hidden_out) {
     st = hip_check(hipMemcpyAsync(hidden_out, hf, (size_t)n_rows * c.d_model * 2, hipMemcpyDeviceToDevice, stream),
                    "hipMemcpyAsync(hidden_out)");

@@ -35,7 +35,7 @@ __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, 
 struct EpiResid {
   float* r;
   template <int SW, int ST>
-  __device__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -57,7 +57,7 @@ struct EpiResid {
 struct EpiSwiglu {
   bf16_t* a;  // [T, Nw/2]
   template <int SW, int ST>
-  __device__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
     const int F = Nw >> 1;
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
@@ -80,7 +80,7 @@ struct EpiSwiglu {
 struct EpiQkv {
   QkvOut o;
   template <int SW, int ST>
-  __device__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
     const int dh = o.dh, half = dh >> 1;
     const int qrows = o.H * dh, krows = o.Hkv * dh;
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
@@ -129,7 +129,7 @@ struct EpiQkv {
 struct EpiF32 {
   float* out;
   template <int SW, int ST>
-  __device__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -183,7 +183,7 @@ template <int BW, int WW>
 struct EpiLm {
   LmOut o;
   template <int SW, int ST>
-  __device__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int tile_w) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int tile_w) const {
     __shared__ Part xch[WW][256];  // [wave along W][token within the workgroup tile]; BT <= 256
     const int wid = threadIdx.x >> 6;
     const int wave_w = wid % WW, wave_t = wid / WW;
@@ -205,7 +205,7 @@ struct EpiLm {
         x.m1 = __shfl_xor(p.m1, off, 64); x.m2 = __shfl_xor(p.m2, off, 64);
         x.i1 = __shfl_xor(p.i1, off, 64); x.i2 = __shfl_xor(p.i2, off, 64);
         x.s = 0.f;
-        Part y = (lane & off) ? part_merge(x, p) : part_merge(p, x);
+        Part y = part_merge(p, x);  // symmetric: ids differ, so argument order does not matter
         p.m1 = y.m1; p.m2 = y.m2; p.i1 = y.i1; p.i2 = y.i2;
       }
       float s = 0.f;
@@ -249,32 +249,92 @@ struct EpiLm {
 };
 
 // ---------------------------------------------------------------- the kernel
-template <int BW, int BT, int WW, int WT, class Epi>
-__global__ void __launch_bounds__(WW * WT * 64)
-gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
-            const int32_t* __restrict__ t_count, Epi epi) {
-  constexpr int NT = WW * WT * 64, TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
-  constexpr int WCH = BW * 8, XCH = BT * 8;  // 16-byte chunks per stage
-  constexpr int WPT = (WCH + NT - 1) / NT, XPT = (XCH + NT - 1) / NT;
-  static_assert(TW % 16 == 0 && TT % 16 == 0, "wave tile must be a multiple of 16");
-  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
-  bf16_t* sW = smem;                      // [2][BW * LDSP]
-  bf16_t* sX = smem + 2 * BW * LDSP;      // [2][BT * LDSP]
+// Direct-to-LDS multi-stage pipeline: each stage holds a BW x 64 weight slice and a BT x 64
+// activation slice, written by global_load_lds_dwordx4 (16 bytes per lane straight into LDS, no
+// register staging). Rows are 8 chunks of 16 bytes, XOR-swizzled (chunk c of row r at c ^ (r & 7))
+// so the MFMA fragment reads are bank-conflict free. Loads for stage k + STAGES - 1 are issued while
+// stage k is computed; vmcnt waits count only this wave's own outstanding stages, and a bare
+// s_barrier (no vmcnt(0) fence) publishes the stage to the other waves.
+//
+// Split-K: unit (tile, split) accumulates K-steps [split*per, ...). With nsplit > 1 every unit
+// writes its float32 partial to the workspace and increments the tile's counter; the last unit to
+// arrive adds the partials in split order (fixed, so results are bitwise reproducible), resets the
+// counter and runs the epilogue. No unit waits on another.
+__device__ __attribute__((aligned(64))) uint4 g_zero_chunk[4];
 
-  // XCD-aware tile order: XCD x (= blockIdx % 8) walks a contiguous run of logical tiles; tiles
-  // adjacent in that run share the weight tile and differ in the token tile.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int BW, int BT, int STAGES, class Epi>
+__global__ void __launch_bounds__(256)
+gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
+            const int32_t* __restrict__ t_count, int nsplit, float* __restrict__ partials,
+            int32_t* __restrict__ counters, Epi epi) {
+  constexpr int WW = 2, WT = 2, NT = 256, NWAVE = 4;
+  constexpr int TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
+  constexpr int CH = (BW + BT) * 8;     // 16-byte chunks per stage
+  constexpr int IPW = CH / 64 / NWAVE;  // load instructions per wave per stage
+  static_assert(TW % 16 == 0 && TT % 16 == 0 && CH % (64 * NWAVE) == 0 && (BW * 8) % 64 == 0, "tile shape");
+  static_assert(STAGES >= 2 && IPW * (STAGES - 2) < 64, "pipeline depth");
+  extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
+
   const int nW = (Nw + BW - 1) / BW, nTt = (T + BT - 1) / BT;
-  const int total = nW * nTt;
-  const int per = (total + 7) / 8;
+  const int tiles = nW * nTt, units = tiles * nsplit;
+  const int per = (units + 7) / 8;
   const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
-  if (L >= total) return;
-  const int tile_w = L / nTt, tile_t = L - tile_w * nTt;
+  if (L >= units) return;
+  // unit order: weight tile, then split, then token tile (neighbours share a weight slice)
+  const int tile_t = L % nTt, rest = L / nTt;
+  const int split = rest % nsplit, tile_w = rest / nsplit;
+  const int tile = tile_w * nTt + tile_t;
   const int w0 = tile_w * BW, t0 = tile_t * BT;
-  const int Tv = t_count ? min(T, *t_count) : T;  // valid token rows
-  if (t0 >= Tv) return;
+  const int Tv = t_count ? min(T, *t_count) : T;
+  if (t0 >= Tv) return;  // every split of this tile leaves here: the tile is never finalised
+
+  const int nk_all = (K + 63) / 64;
+  const int kper = (nk_all + nsplit - 1) / nsplit;
+  const int kb = min(nk_all, split * kper);
+  const int nk = min(nk_all, kb + kper) - kb;
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wave_w = wid % WW, wave_t = wid / WW;
+
+  // Per-lane element offset of this wave's load instructions (loop invariant; -1 = row outside the
+  // operand). Instruction i of wave `wid` fills chunks [(wid*IPW + i)*64, +64) of the stage: all of
+  // them weight chunks or all activation chunks, so the operand choice is wave-uniform.
+  int off[IPW];
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int q = wid * IPW + i;
+    const int pos = q * 64 + lane;
+    const bool isw = q * 64 < BW * 8;
+    const int p2 = isw ? pos : pos - BW * 8;
+    const int row = p2 >> 3, c = (p2 & 7) ^ (row & 7);
+    const int grow = (isw ? w0 : t0) + row;
+    off[i] = (grow < (isw ? Nw : Tv)) ? grow * K + c * 8 : -1;
+  }
+  const bool ktail = (K & 63) != 0;
+  auto issue = [&](int kt) {
+    uint4* stage = sm + (kt % STAGES) * CH;
+    const int k0 = (kb + kt) * 64;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int q = wid * IPW + i;
+      const bf16_t* base = (q * 64 < BW * 8) ? W : X;
+      bool ok = off[i] >= 0;
+      if (ktail) {
+        const int p2 = (q * 64 < BW * 8 ? q * 64 : q * 64 - BW * 8) + lane;
+        ok = ok && k0 + ((p2 & 7) ^ ((p2 >> 3) & 7)) * 8 < K;
+      }
+      const void* g = ok ? static_cast<const void*>(base + (size_t)off[i] + k0) : static_cast<const void*>(g_zero_chunk);
+      __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(stage + q * 64), 16, 0, 0);
+    }
+  };
 
   f32x4_t acc[SW][ST];
 #pragma unroll
@@ -282,113 +342,181 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
 #pragma unroll
     for (int j = 0; j < ST; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  uint4 rw[WPT], rx[XPT];
-  auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < WPT; ++i) {
-      const int c = tid + i * NT;
-      const int row = c >> 3, col = (c & 7) * 8;
-      const int gr = w0 + row, gk = k0 + col;
-      rw[i] = (c < WCH && gr < Nw && gk < K) ? *reinterpret_cast<const uint4*>(W + (size_t)gr * K + gk)
-                                             : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < XPT; ++i) {
-      const int c = tid + i * NT;
-      const int row = c >> 3, col = (c & 7) * 8;
-      const int gt = t0 + row, gk = k0 + col;
-      rx[i] = (c < XCH && gt < Tv && gk < K) ? *reinterpret_cast<const uint4*>(X + (size_t)gt * K + gk)
-                                             : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < WPT; ++i) {
-      const int c = tid + i * NT;
-      if (c < WCH) *reinterpret_cast<uint4*>(sW + buf * BW * LDSP + (c >> 3) * LDSP + (c & 7) * 8) = rw[i];
-    }
-#pragma unroll
-    for (int i = 0; i < XPT; ++i) {
-      const int c = tid + i * NT;
-      if (c < XCH) *reinterpret_cast<uint4*>(sX + buf * BT * LDSP + (c >> 3) * LDSP + (c & 7) * 8) = rx[i];
-    }
-  };
-
-  const int nk = (K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int frag_row = lane & 15, frag_k = 8 * (lane >> 4);
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) issue(st);
+  const int frow = lane & 15, fchunk = lane >> 4;
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const bf16_t* cW = sW + cur * BW * LDSP + (wave_w * TW + frag_row) * LDSP + frag_k;
-    const bf16_t* cX = sX + cur * BT * LDSP + (wave_t * TT + frag_row) * LDSP + frag_k;
+    // stages issued but not yet needed after this one: min(STAGES - 2, nk - 1 - kt)
+    const int pending = min(STAGES - 2, nk - 1 - kt);
+    if (STAGES >= 4 && pending >= 2) wait_vmcnt<(STAGES >= 4 ? 2 : 0) * IPW>();
+    else if (pending >= 1) wait_vmcnt<IPW>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const uint4* stage = sm + (kt % STAGES) * CH;
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = 4 * ks + fchunk;
       bf16x8_t a[SW], b[ST];
 #pragma unroll
-      for (int i = 0; i < SW; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(cW + 16 * i * LDSP + 32 * ks);
+      for (int i = 0; i < SW; ++i) {
+        const int r = wave_w * TW + 16 * i + frow;
+        a[i] = __builtin_bit_cast(bf16x8_t, stage[r * 8 + (c ^ (r & 7))]);
+      }
 #pragma unroll
-      for (int j = 0; j < ST; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(cX + 16 * j * LDSP + 32 * ks);
+      for (int j = 0; j < ST; ++j) {
+        const int r = wave_t * TT + 16 * j + frow;
+        b[j] = __builtin_bit_cast(bf16x8_t, stage[BW * 8 + r * 8 + (c ^ (r & 7))]);
+      }
 #pragma unroll
       for (int i = 0; i < SW; ++i)
 #pragma unroll
         for (int j = 0; j < ST; ++j) acc[i][j] = mfma16(a[i], b[j], acc[i][j]);
     }
-    if (kt + 1 < nk) sstore(cur ^ 1);
+  }
+
+  if (nsplit > 1) {
+    __shared__ int s_last;
+    f32x4_t* slots = reinterpret_cast<f32x4_t*>(partials);
+    constexpr size_t SLOT = (size_t)SW * ST * NT;  // float4 per unit
+    f32x4_t* mine = slots + ((size_t)tile * nsplit + split) * SLOT;
+#pragma unroll
+    for (int i = 0; i < SW; ++i)
+#pragma unroll
+      for (int j = 0; j < ST; ++j) mine[(i * ST + j) * NT + tid] = acc[i][j];
+    __threadfence();
     __syncthreads();
+    if (tid == 0) s_last = (atomicAdd(&counters[tile], 1) == nsplit - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    f32x4_t tot[SW][ST];
+#pragma unroll
+    for (int i = 0; i < SW; ++i)
+#pragma unroll
+      for (int j = 0; j < ST; ++j) tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const f32x4_t* other = slots + ((size_t)tile * nsplit + sp) * SLOT;
+#pragma unroll
+      for (int i = 0; i < SW; ++i)
+#pragma unroll
+        for (int j = 0; j < ST; ++j) tot[i][j] += (sp == split) ? acc[i][j] : other[(i * ST + j) * NT + tid];
+    }
+    if (tid == 0) counters[tile] = 0;  // ready for the next launch
+    epi.template apply<SW, ST>(tot, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+    return;
   }
   epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
 }
 
-// ---------------------------------------------------------------- dispatch
-template <int BW, int BT, int WW, int WT, class Epi>
-static void run_gemm(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, const Epi& epi,
-                     hipStream_t s) {
-  const int nW = (Nw + BW - 1) / BW, nTt = (T + BT - 1) / BT;
-  const int total = nW * nTt;
-  if (total == 0) return;
-  const int grid = 8 * ((total + 7) / 8);
-  const size_t lds = (size_t)2 * (BW + BT) * LDSP * sizeof(bf16_t);
-  auto kern = gemm_kernel<BW, BT, WW, WT, Epi>;
-  static bool attr_set = false;  // one kernel per instantiation; raise the dynamic-LDS cap once
+// ---------------------------------------------------------------- planning and dispatch
+struct TileCfg {
+  int bw, bt, stages;
+};
+static const TileCfg kCfgs[] = {
+    {128, 128, 4}, {96, 192, 4}, {192, 192, 3}, {128, 96, 4}, {128, 64, 4}, {128, 256, 3}, {64, 64, 4},
+};
+constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
+constexpr int kCUs = 256;
+
+static size_t cfg_lds(const TileCfg& c) { return (size_t)c.stages * (c.bw + c.bt) * 8 * 16; }
+
+// Estimated time of one GEMM under a tile shape and split count: whole rounds of 256 units, each
+// unit costing its MACs scaled by a fragment-reuse efficiency, plus the partial-sum traffic.
+static double plan_cost(const TileCfg& c, int n, int Nw, int T, int K) {
+  const double tiles = (double)((Nw + c.bw - 1) / c.bw) * ((T + c.bt - 1) / c.bt);
+  const double units = tiles * n;
+  const double rounds = ceil(units / kCUs);
+  const double sw = c.bw / 32.0, st = c.bt / 32.0;
+  const double eff = sw * st / (sw * st + 0.5 * (sw + st));
+  const double mac_rate = 2.5e15 / 2 / kCUs;  // MAC/s per CU at the bf16 peak
+  const double t_unit = (double)c.bw * c.bt * ((double)K / n) / eff / mac_rate;
+  const double t_part = n > 1 ? 2.0 * (n - 1) * (double)T * Nw * 4 / 6e12 : 0.0;
+  const double t_pipe = 4 * 64 * 1e-9 * ((double)K / 64 / n > 0 ? 1 : 0);  // pipeline fill
+  return rounds * (t_unit + t_pipe) + t_part;
+}
+
+GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
+  GemmPlan best{0, 1, 0};
+  double best_t = 1e30;
+  const int nk = (K + 63) / 64;
+  for (int ci = 0; ci < kNumCfgs; ++ci) {
+    if (force_bw && kCfgs[ci].bw != force_bw) continue;
+    for (int n = 1; n <= max_split; ++n) {
+      if (n > 1 && nk / n < 8) break;
+      const double t = plan_cost(kCfgs[ci], n, Nw, T, K);
+      if (t < best_t * 0.999) {
+        best_t = t;
+        best.cfg = ci;
+        best.nsplit = n;
+      }
+    }
+  }
+  const TileCfg& c = kCfgs[best.cfg];
+  best.tiles = ((Nw + c.bw - 1) / c.bw) * ((T + c.bt - 1) / c.bt);
+  return best;
+}
+
+size_t gemm_partial_bytes(const GemmPlan& p) {
+  if (p.nsplit <= 1) return 0;
+  const TileCfg& c = kCfgs[p.cfg];
+  return (size_t)p.tiles * p.nsplit * c.bw * c.bt * 4;
+}
+
+template <int BW, int BT, int STAGES, class Epi>
+static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
+                    const GemmScratch& sc, const Epi& epi, hipStream_t s) {
+  const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
+  const int units = tiles * nsplit;
+  if (units == 0) return;
+  const int grid = 8 * ((units + 7) / 8);
+  const size_t lds = (size_t)STAGES * (BW + BT) * 8 * 16;
+  auto kern = gemm_kernel<BW, BT, STAGES, Epi>;
+  static bool attr_set = false;  // one flag per instantiation
   if (!attr_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, epi);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, W, X, Nw, T, K, t_count, nsplit, sc.partials, sc.counters,
+                     epi);
 }
 
-// Tile choice: the large 128x128 tile when it yields enough workgroups to cover the 256 CUs,
-// otherwise 128 weight rows x 64 tokens.
 template <class Epi>
-static void gemm_auto(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const Epi& epi, hipStream_t s) {
-  const long big = (long)((Nw + 127) / 128) * ((T + 127) / 128);
-  if (T > 64 && big >= 240)
-    run_gemm<128, 128, 2, 2>(W, X, Nw, T, K, nullptr, epi, s);
-  else
-    run_gemm<128, 64, 2, 2>(W, X, Nw, T, K, nullptr, epi, s);
+static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
+                     const GemmScratch& sc, const Epi& epi, hipStream_t s) {
+  switch (p.cfg) {
+    case 0: run_cfg<128, 128, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 1: run_cfg<96, 192, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 2: run_cfg<192, 192, 3>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 3: run_cfg<128, 96, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 4: run_cfg<128, 64, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 5: run_cfg<128, 256, 3>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    default: run_cfg<64, 64, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+  }
 }
 
-void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, hipStream_t s) {
-  gemm_auto(W, X, Nw, T, K, EpiQkv{o}, s);
+void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, const GemmScratch& sc,
+              hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 4), W, X, Nw, T, K, nullptr, sc, EpiQkv{o}, s);
 }
-void gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, hipStream_t s) {
-  gemm_auto(W, X, Nw, T, K, EpiResid{r}, s);
+void gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, const GemmScratch& sc,
+                hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 4), W, X, Nw, T, K, nullptr, sc, EpiResid{r}, s);
 }
-void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, hipStream_t s) {
-  gemm_auto(W, X, Nw, T, K, EpiSwiglu{a}, s);
+void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, const GemmScratch& sc,
+                 hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 4), W, X, Nw, T, K, nullptr, sc, EpiSwiglu{a}, s);
 }
-void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, hipStream_t s) {
-  gemm_auto(W, X, Nw, T, K, EpiF32{out}, s);
+void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, const GemmScratch& sc,
+                    hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiF32{out}, s);
 }
-void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, hipStream_t s) {
-  static_assert(kLmTile == 128, "LM-head tile is the GEMM's BW");
-  if (T > 64)
-    run_gemm<128, 128, 2, 2>(W, X, V, T, K, o.count, EpiLm<128, 2>{o}, s);
-  else
-    run_gemm<128, 64, 2, 2>(W, X, V, T, K, o.count, EpiLm<128, 2>{o}, s);
+void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, const GemmScratch& sc,
+                 hipStream_t s) {
+  static_assert(kLmTile == 128, "the LM-head vocabulary tile is the GEMM's weight tile");
+  run_plan(plan_gemm(V, T, K, kLmTile, 1), W, X, V, T, K, o.count, sc, EpiLm<128, 2>{o}, s);
 }
 
 }  // namespace dcl

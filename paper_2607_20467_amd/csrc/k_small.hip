@@ -9,11 +9,14 @@ namespace dcl {
 
 // ---------------------------------------------------------------- embedding gather
 // r[t, :] = E[tokens[t], :] widened to float32; ids outside [0, V) give a zero row.
+// The first n_zero threads also clear the split-K arrival counters of the step's GEMMs.
 __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ tokens,
                                                    const bf16_t* __restrict__ E, float* __restrict__ r,
-                                                   int T, int d, int V) {
+                                                   int T, int d, int V, int32_t* __restrict__ zero_cnt,
+                                                   int n_zero) {
   const int chunks = d / 8;
   long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < n_zero) zero_cnt[idx] = 0;
   if (idx >= (long)T * chunks) return;
   int t = (int)(idx / chunks), c = (int)(idx % chunks);
   int id = tokens[t];
@@ -30,10 +33,13 @@ __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ 
   dst[1] = hi;
 }
 
-void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, hipStream_t s) {
+void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, int32_t* zero_cnt,
+                  int n_zero, hipStream_t s) {
   long n = (long)T * (d / 8);
+  if (n < n_zero) n = n_zero;
   if (n == 0) return;
-  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tokens, E, r, T, d, V);
+  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tokens, E, r, T, d, V, zero_cnt,
+                     n_zero);
 }
 
 // ---------------------------------------------------------------- RMSNorm
@@ -177,8 +183,7 @@ __global__ void __launch_bounds__(256) merge_kernel(const float* __restrict__ pm
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     Top2 x = {__shfl_xor(t.m1, o, 64), __shfl_xor(t.m2, o, 64), __shfl_xor(t.i1, o, 64), __shfl_xor(t.i2, o, 64)};
-    // keep the operand order fixed (lower lane first) so every lane computes the same result
-    t = (lane & o) ? top2_merge(x, t) : top2_merge(t, x);
+    t = top2_merge(t, x);  // symmetric (distinct ids), so every lane computes the same result
   }
   const float M = t.m1;
   float s = 0.f;
@@ -204,14 +209,17 @@ void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const 
 }
 
 // rows[j] = j for j < n, count = n (row map of dcl_score_hidden and dcl_debug_logits' copy).
-__global__ void iota_kernel(int32_t* __restrict__ rows, int32_t* __restrict__ count, int n) {
+__global__ void iota_kernel(int32_t* __restrict__ rows, int32_t* __restrict__ count, int n,
+                            int32_t* __restrict__ zero_cnt, int n_zero) {
   int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j < n) rows[j] = j;
   if (j == 0) *count = n;
+  if (j < n_zero) zero_cnt[j] = 0;
 }
 
-void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s) {
-  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, rows, count, n);
+void launch_iota(int32_t* rows, int32_t* count, int n, int32_t* zero_cnt, int n_zero, hipStream_t s) {
+  const int m = n > n_zero ? n : n_zero;
+  hipLaunchKernelGGL(iota_kernel, dim3((m + 255) / 256), dim3(256), 0, s, rows, count, n, zero_cnt, n_zero);
 }
 
 // ---------------------------------------------------------------- DCV + drafts + remask

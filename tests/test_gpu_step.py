@@ -38,6 +38,11 @@ CASES = {
     "wide": _variant("wide", _W["c1s"], dict(n_layers=3, d_model=512, n_heads=8, n_kv_heads=8, d_ffn=1376,
                                              vocab=8192, mask_id=8191, weight_dtype="bf16"),
                      batch=1, prompt_len=96, gen_len=224, window=32, p=96, draft=(128, 192)),
+    # full LLaDA-8B width and vocabulary, 2 of its 32 layers: the tile plans and split-K of the
+    # 384-token step (B1, 128 prompt + 256 generation), the 126464-id LM head
+    "llada_2l": _variant("llada_2l", _W["c2"], dict(n_layers=2)),
+    # full Dream-7B width and vocabulary (GQA 28/4, biases), 2 of 28 layers, B2 x 384 tokens
+    "dream_2l": _variant("dream_2l", _W["c4"], dict(n_layers=2), batch=2, prompt_len=128, gen_len=256),
 }
 
 _cache = {}
@@ -62,7 +67,7 @@ def test_step_parity(key):
     compare_stats(stats_to_np(st), ref, w.tau_commit, w.tau_draft, what=key, conf_tol=ct, logit_tol=lt)
 
 
-@pytest.mark.parametrize("key", ["c1", "c1s", "ragged", "gqa_bias_dh128", "wide"])
+@pytest.mark.parametrize("key", ["c1", "c1s", "ragged", "gqa_bias_dh128", "wide", "llada_2l"])
 def test_lm_head_on_gpu_hidden_exact_bar(key):
     """Exact-input stage: the GPU's float32 logits equal h_f W_lm^T (float64) of the GPU's own bf16 final
     hidden states within 2e-2, and those hidden states stay close to the oracle's."""
@@ -85,7 +90,7 @@ def test_lm_head_on_gpu_hidden_exact_bar(key):
     assert rel.max() < 0.1
 
 
-@pytest.mark.parametrize("key", ["c1", "ragged", "wide"])
+@pytest.mark.parametrize("key", ["c1", "ragged", "wide", "llada_2l", "dream_2l"])
 def test_score_hidden_exact_bar(key):
     """dcl_score_hidden (fused LM head + vocabulary reduction) on synthetic bf16 hidden rows vs the oracle's
     materialised softmax: conf within 1e-3, lse within 2e-2, ids exact except near-ties."""
@@ -176,13 +181,16 @@ def test_full_loop_matches_oracle_every_iteration():
     st = run.new_stats(B, S)
     n = 0
     p_host = p.cpu().numpy()
+    # tolerance sized once on the full initial state (96 scored rows): the drift of a late state with
+    # only a few scored rows is too small a sample to bound the GPU's
+    ref0 = oracle.step(w.geom, W, x, p_host, S)
+    ct, lt = derived_tolerance(w.geom, W, x, p_host, S, ref0)
     while (p_host < S).any():
         assert n < M, "loop exceeded M iterations"
         x_before, p_before = tok.cpu().numpy(), p_host
         run.step(tok, p, S, stats=st)
         g = stats_to_np(st)
         ref = oracle.step(w.geom, W, x_before, p_before, S)
-        ct, lt = derived_tolerance(w.geom, W, x_before, p_before, S, ref)
         compare_stats(g, ref, tc, td, what=f"iteration {n}", conf_tol=ct, logit_tol=lt)
         dcl.dcl_select_contiguous(tok, B, S, p, S, L, tc, td, w.geom.mask_id, st)
         x_ref, p_ref, _, _ = oracle.select_contiguous(x_before, p_before, S, L, tc, td, w.geom.mask_id, g["top1"],
