@@ -50,7 +50,7 @@ typedef enum {
 
 /* Model geometry: a pre-norm bidirectional transformer with RMSNorm, rotate-half RoPE, SwiGLU
  * (the LLaDA / Dream base models of Section 4 setup). Host struct. Supported: head_dim 64 or
- * 128; n_heads % n_kv_heads == 0; d_model, d_ffn multiples of 16; vocab >= 2;
+ * 128; n_heads % n_kv_heads == 0; d_model, d_ffn multiples of 16 (d_model <= 8192); vocab >= 2;
  * 0 <= mask_id < vocab; rms_eps > 0; rope_base > 1; 1 <= max_positions <= 65536. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab, mask_id;

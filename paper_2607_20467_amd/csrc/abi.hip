@@ -39,7 +39,8 @@ dcl_status check_config(const dcl_config* c) {
   if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads != 0)
     return fail(DCL_E_UNSUPPORTED, "n_heads %d must be a positive multiple of n_kv_heads %d", c->n_heads,
                 c->n_kv_heads);
-  if (c->d_model < 16 || c->d_model % 16 != 0) return fail(DCL_E_UNSUPPORTED, "d_model %d must be a multiple of 16", c->d_model);
+  if (c->d_model < 16 || c->d_model % 16 != 0 || c->d_model > 8192)
+    return fail(DCL_E_UNSUPPORTED, "d_model %d must be a multiple of 16, at most 8192", c->d_model);
   if (c->d_ffn < 16 || c->d_ffn % 16 != 0) return fail(DCL_E_UNSUPPORTED, "d_ffn %d must be a multiple of 16", c->d_ffn);
   if ((long)c->n_heads * c->head_dim > (1 << 20)) return fail(DCL_E_ARG, "n_heads * head_dim too large");
   if (c->vocab < 2) return fail(DCL_E_ARG, "vocab %d < 2", c->vocab);
@@ -112,8 +113,8 @@ StepLayout step_layout(const dcl_config& c, int B, int S) {
   L.ps = take(np);
   // split-K scratch of the four per-layer GEMMs (their shapes are fixed by B*S)
   const int Ti = (int)T, qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
-  const GemmPlan plans[4] = {plan_gemm(qkv, Ti, c.d_model, 0, 4), plan_gemm(c.d_model, Ti, c.n_heads * c.head_dim, 0, 4),
-                             plan_gemm(2 * c.d_ffn, Ti, c.d_model, 0, 4), plan_gemm(c.d_model, Ti, c.d_ffn, 0, 4)};
+  const GemmPlan plans[4] = {plan_gemm(qkv, Ti, c.d_model, 0, 1), plan_gemm(c.d_model, Ti, c.n_heads * c.head_dim, 0, 1),
+                             plan_gemm(2 * c.d_ffn, Ti, c.d_model, 0, 1), plan_gemm(c.d_model, Ti, c.d_ffn, 0, 1)};
   size_t part = 0;
   int ntile = 1;
   for (const GemmPlan& gp : plans) {

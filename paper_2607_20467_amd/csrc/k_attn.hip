@@ -17,17 +17,31 @@ namespace dcl {
 
 constexpr int KT = 64;  // keys per tile
 
+__device__ __attribute__((aligned(64))) uint4 g_attn_zero[4];
+
 __device__ __forceinline__ f32x4_t mfma16a(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-template <int NW, int DH>
+template <int N>
+__device__ __forceinline__ void attn_wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// K and V^T tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 into a STAGES-deep ring (no
+// register staging, no padding). K rows (DH/8 chunks of 16 bytes) are XOR-swizzled by the key
+// index, V^T rows (8 chunks = 64 keys) by the dimension index, so the fragment reads below are
+// bank-conflict free. Chunks past the last key read a zero chunk.
+template <int NW, int DH, int STAGES>
 __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   constexpr int BQ = 16 * NW, NT = NW * 64;
-  constexpr int KP = DH + 8;  // padded K row (keys x dims)
-  constexpr int VP = KT + 8;  // padded V^T row (dims x keys)
-  __shared__ __attribute__((aligned(16))) bf16_t sK[KT * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[DH * VP];
+  constexpr int KC = DH / 8;           // chunks per K row
+  constexpr int KCH = KT * KC;         // K chunks per stage
+  constexpr int VCH = DH * (KT / 8);   // V^T chunks per stage
+  constexpr int SCH = KCH + VCH;       // chunks per stage
+  constexpr int IPW = SCH / 64 / NW;   // load instructions per wave per stage
+  static_assert(SCH % (64 * NW) == 0 && KCH % 64 == 0, "stage shape");
+  extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
 
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int g = h / (a.H / a.Hkv);
@@ -35,8 +49,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   const int lq = lane & 15, lg = lane >> 4;
   const int S = a.S, P = a.P, nkeys = P + S;
   const int qrow = qt * BQ + wid * 16 + lq;
+  const int ntiles = (nkeys + KT - 1) / KT;
 
-  // Q fragments (B operand): query lq, dims [32 ks + 8 lg, +8)
   bf16x8_t qf[DH / 32];
   {
     const bf16_t* qp = a.q + (((size_t)b * a.H + h) * S + (qrow < S ? qrow : 0)) * DH + 8 * lg;
@@ -52,51 +66,61 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   const bf16_t* vc = a.vc ? a.vc + kvh * DH * P : nullptr;
   const bf16_t* vf = a.vt + kvh * DH * a.Sp;
 
+  auto issue = [&](int t) {
+    uint4* stage = sm + (t % STAGES) * SCH;
+    const int k0 = t * KT;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int q = wid * IPW + i;
+      const int pos = q * 64 + lane;
+      const void* src = g_attn_zero;
+      if (q * 64 < KCH) {  // K chunk: slot pos -> key row, chunk column
+        const int key = pos / KC, slot = pos % KC;
+        const int c = slot ^ (key & (KC - 1));
+        const int j = k0 + key;
+        if (j < P) src = kc + (size_t)j * DH + c * 8;
+        else if (j < nkeys) src = kf + (size_t)(j - P) * DH + c * 8;
+      } else {             // V^T chunk: slot -> dimension row, 8-key chunk
+        const int p2 = pos - KCH;
+        const int d = p2 >> 3, slot = p2 & 7;
+        const int c = slot ^ (d & 7);
+        const int j = k0 + c * 8;
+        if (j < P) src = vc + (size_t)d * P + j;
+        else if (j < nkeys) src = vf + (size_t)d * a.Sp + (j - P);
+      }
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(stage + q * 64), 16, 0, 0);
+    }
+  };
+
   f32x4_t o[DH / 16];
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
 
-  for (int k0 = 0; k0 < nkeys; k0 += KT) {
-    // K tile [KT keys][DH]
 #pragma unroll
-    for (int c = tid; c < KT * DH / 8; c += NT) {
-      const int key = c / (DH / 8), col = (c % (DH / 8)) * 8, j = k0 + key;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (j < P) v = *reinterpret_cast<const uint4*>(kc + (size_t)j * DH + col);
-      else if (j < nkeys) v = *reinterpret_cast<const uint4*>(kf + (size_t)(j - P) * DH + col);
-      *reinterpret_cast<uint4*>(sK + key * KP + col) = v;
-    }
-    // V^T tile [DH][KT keys]; P % 8 == 0 and Sp % 8 == 0 keep every full 8-key chunk in one source
-#pragma unroll
-    for (int c = tid; c < DH * KT / 8; c += NT) {
-      const int d = c / (KT / 8), kk = (c % (KT / 8)) * 8, j = k0 + kk;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (j + 8 <= nkeys) {
-        v = (j < P) ? *reinterpret_cast<const uint4*>(vc + (size_t)d * P + j)
-                    : *reinterpret_cast<const uint4*>(vf + (size_t)d * a.Sp + (j - P));
-      } else if (j < nkeys) {
-        uint16_t e[8];
-#pragma unroll
-        for (int x = 0; x < 8; ++x) {
-          const int jj = j + x;
-          e[x] = jj >= nkeys ? 0 : (jj < P ? vc[(size_t)d * P + jj] : vf[(size_t)d * a.Sp + (jj - P)]);
-        }
-        v = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16));
-      }
-      *reinterpret_cast<uint4*>(sV + d * VP + kk) = v;
-    }
-    __syncthreads();
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < ntiles) issue(st);
+  for (int t = 0; t < ntiles; ++t) {
+    const int pending = min(STAGES - 2, ntiles - 1 - t);
+    if (STAGES >= 3 && pending >= 1) attn_wait_vmcnt<(STAGES >= 3 ? IPW : 0)>();
+    else attn_wait_vmcnt<0>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (t + STAGES - 1 < ntiles) issue(t + STAGES - 1);
+    const uint4* sK = sm + (t % STAGES) * SCH;
+    const uint4* sV = sK + KCH;
+    const int k0 = t * KT;
 
     // S^T = K Q^T: lane holds keys 16 kt + 4 lg + r of query lq
     f32x4_t sc[KT / 16];
 #pragma unroll
     for (int kt = 0; kt < KT / 16; ++kt) {
       sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      const bf16_t* kp = sK + (16 * kt + lq) * KP + 8 * lg;
+      const int row = 16 * kt + lq;
 #pragma unroll
-      for (int ks = 0; ks < DH / 32; ++ks)
-        sc[kt] = mfma16a(*reinterpret_cast<const bf16x8_t*>(kp + 32 * ks), qf[ks], sc[kt]);
+      for (int ks = 0; ks < DH / 32; ++ks) {
+        const int c = 4 * ks + lg;
+        sc[kt] = mfma16a(__builtin_bit_cast(bf16x8_t, sK[row * KC + (c ^ (row & (KC - 1)))]), qf[ks], sc[kt]);
+      }
     }
     float tmax = -INFINITY;
 #pragma unroll
@@ -141,17 +165,18 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
       }
       const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
       const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+      const int c0 = 4 * s2 + (lg >> 1), c1 = c0 + 2, half = lg & 1;
 #pragma unroll
       for (int dt = 0; dt < DH / 16; ++dt) {
-        const bf16_t* vp = sV + (16 * dt + lq) * VP + 32 * s2 + 4 * lg;
-        const uint2 v0 = *reinterpret_cast<const uint2*>(vp);
-        const uint2 v1 = *reinterpret_cast<const uint2*>(vp + 16);
+        const int d = 16 * dt + lq;
+        const uint2* r0 = reinterpret_cast<const uint2*>(sV + d * 8 + (c0 ^ (d & 7))) + half;
+        const uint2* r1 = reinterpret_cast<const uint2*>(sV + d * 8 + (c1 ^ (d & 7))) + half;
+        const uint2 v0 = *r0, v1 = *r1;
         const bf16x8_t va = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
         o[dt] = mfma16a(va, phi, o[dt]);
         o[dt] = mfma16a(va, plo, o[dt]);
       }
     }
-    __syncthreads();
   }
 
   if (qrow < S) {
@@ -167,21 +192,31 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   }
 }
 
-template <int NW>
+template <int NW, int STAGES>
 static void run_attn(const AttnArgs& a, hipStream_t s) {
   dim3 grid((a.S + 16 * NW - 1) / (16 * NW), a.H, a.B);
-  if (a.dh == 128)
-    hipLaunchKernelGGL((attn_kernel<NW, 128>), grid, dim3(NW * 64), 0, s, a);
-  else
-    hipLaunchKernelGGL((attn_kernel<NW, 64>), grid, dim3(NW * 64), 0, s, a);
+  const size_t lds = (size_t)STAGES * (KT * (a.dh / 8) + a.dh * (KT / 8)) * 16;
+  if (a.dh == 128) {
+    auto kern = attn_kernel<NW, 128, STAGES>;
+    static bool set = false;
+    if (!set) {
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      set = true;
+    }
+    hipLaunchKernelGGL(kern, grid, dim3(NW * 64), lds, s, a);
+  } else {
+    auto kern = attn_kernel<NW, 64, STAGES>;
+    static bool set = false;
+    if (!set) {
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      set = true;
+    }
+    hipLaunchKernelGGL(kern, grid, dim3(NW * 64), lds, s, a);
+  }
 }
 
-void launch_attention(const AttnArgs& a, hipStream_t s) {
-  const long blocks4 = (long)((a.S + 63) / 64) * a.H * a.B;
-  if (blocks4 >= 512)
-    run_attn<4>(a, s);
-  else
-    run_attn<2>(a, s);
-}
+// Four wavefronts (64 queries) per workgroup and a two-stage ring: fastest for every LLaDA / Dream
+// attention shape measured on MI355X (S 384-1280, 64 queries over a 1216-key prefix).
+void launch_attention(const AttnArgs& a, hipStream_t s) { run_attn<4, 2>(a, s); }
 
 }  // namespace dcl

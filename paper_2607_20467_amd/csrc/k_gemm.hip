@@ -120,6 +120,10 @@ struct EpiQkv {
           base[o.Sp] = f2bf(v1);
           base[2 * (size_t)o.Sp] = f2bf(v2);
           base[3 * (size_t)o.Sp] = f2bf(v3);
+          if (s == o.S - 1) {  // the last token also clears the padding keys [S, Sp) of its four rows
+            for (int z = 1; s + z < o.Sp; ++z)
+              for (int rr = 0; rr < 4; ++rr) base[rr * (size_t)o.Sp + z] = 0;
+          }
         }
       }
     }
@@ -270,12 +274,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int BW, int BT, int STAGES, class Epi>
-__global__ void __launch_bounds__(256)
+template <int BW, int BT, int STAGES, int WW, int WT, class Epi>
+__global__ void __launch_bounds__(WW * WT * 64)
 gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
             const int32_t* __restrict__ t_count, int nsplit, float* __restrict__ partials,
             int32_t* __restrict__ counters, Epi epi) {
-  constexpr int WW = 2, WT = 2, NT = 256, NWAVE = 4;
+  constexpr int NWAVE = WW * WT, NT = NWAVE * 64;
   constexpr int TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
   constexpr int CH = (BW + BT) * 8;     // 16-byte chunks per stage
   constexpr int IPW = CH / 64 / NWAVE;  // load instructions per wave per stage
@@ -410,46 +414,233 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
   epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
 }
 
+// Register-prefetch variant: global -> VGPR loads run PF stages ahead of the MFMAs (the data in
+// flight sits in registers, not in LDS), each stage is written into a double-buffered,
+// XOR-swizzled LDS tile just before it is needed. The compiler's vmcnt waits cover exactly the
+// stage being stored. Same unit order, split-K and epilogues as gemm_kernel.
+template <int BW, int BT, int PF, int WW, int WT, class Epi>
+__global__ void __launch_bounds__(WW * WT * 64)
+gemm_rp_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
+               const int32_t* __restrict__ t_count, int nsplit, float* __restrict__ partials,
+               int32_t* __restrict__ counters, Epi epi) {
+  constexpr int NWAVE = WW * WT, NT = NWAVE * 64;
+  constexpr int TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
+  constexpr int CH = (BW + BT) * 8;   // 16-byte chunks per stage
+  constexpr int CPT = CH / NT;        // chunks per thread per stage
+  static_assert(TW % 16 == 0 && TT % 16 == 0 && CH % NT == 0, "tile shape");
+  extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
+
+  const int nW = (Nw + BW - 1) / BW, nTt = (T + BT - 1) / BT;
+  const int tiles = nW * nTt, units = tiles * nsplit;
+  const int per = (units + 7) / 8;
+  const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  if (L >= units) return;
+  const int tile_t = L % nTt, rest = L / nTt;
+  const int split = rest % nsplit, tile_w = rest / nsplit;
+  const int tile = tile_w * nTt + tile_t;
+  const int w0 = tile_w * BW, t0 = tile_t * BT;
+  const int Tv = t_count ? min(T, *t_count) : T;
+  if (t0 >= Tv) return;
+  const int nk_all = (K + 63) / 64;
+  const int kper = (nk_all + nsplit - 1) / nsplit;
+  const int kb = min(nk_all, split * kper);
+  const int nk = min(nk_all, kb + kper) - kb;
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wave_w = wid % WW, wave_t = wid / WW;
+
+  // chunk j of this thread: stage position pos = j * NT + tid; source pointer (null = zero chunk)
+  const bf16_t* src[CPT];
+  int lds_pos[CPT];
+  int kcol[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    const int pos = j * NT + tid;
+    const bool isw = pos < BW * 8;
+    const int p2 = isw ? pos : pos - BW * 8;
+    const int row = p2 >> 3, c = p2 & 7;
+    const int grow = (isw ? w0 : t0) + row;
+    src[j] = (grow < (isw ? Nw : Tv)) ? (isw ? W : X) + (size_t)grow * K + c * 8 : nullptr;
+    kcol[j] = c * 8;
+    lds_pos[j] = (isw ? 0 : BW * 8) + row * 8 + (c ^ (row & 7));
+  }
+  uint4 regs[PF][CPT];
+  auto gload = [&](int set, int kt) {
+    const int k0 = (kb + kt) * 64;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j)
+      regs[set][j] = (src[j] && k0 + kcol[j] < K) ? *reinterpret_cast<const uint4*>(src[j] + k0) : make_uint4(0, 0, 0, 0);
+  };
+  auto sstore = [&](int set, int buf) {
+    uint4* stage = sm + buf * CH;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) stage[lds_pos[j]] = regs[set][j];
+  };
+
+  f32x4_t acc[SW][ST];
+#pragma unroll
+  for (int i = 0; i < SW; ++i)
+#pragma unroll
+    for (int j = 0; j < ST; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int st = 0; st < PF; ++st)
+    if (st < nk) gload(st, st);
+  if (nk > 0) sstore(0, 0);
+  lds_barrier();
+  const int frow = lane & 15, fchunk = lane >> 4;
+  auto compute = [&](int buf) {
+    const uint4* stage = sm + buf * CH;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = 4 * ks + fchunk;
+      bf16x8_t a[SW], b[ST];
+#pragma unroll
+      for (int i = 0; i < SW; ++i) {
+        const int r = wave_w * TW + 16 * i + frow;
+        a[i] = __builtin_bit_cast(bf16x8_t, stage[r * 8 + (c ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int j = 0; j < ST; ++j) {
+        const int r = wave_t * TT + 16 * j + frow;
+        b[j] = __builtin_bit_cast(bf16x8_t, stage[BW * 8 + r * 8 + (c ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < SW; ++i)
+#pragma unroll
+        for (int j = 0; j < ST; ++j) acc[i][j] = mfma16(a[i], b[j], acc[i][j]);
+    }
+  };
+  // main loop, unrolled by PF so register-set indices are compile-time constants
+  for (int kt0 = 0; kt0 < nk; kt0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int kt = kt0 + u;
+      if (kt < nk) {
+        if (kt + PF < nk) gload(u, kt + PF);          // set u held stage kt, already in LDS
+        compute(kt & 1);
+        if (kt + 1 < nk) sstore((u + 1) % PF, (kt + 1) & 1);
+        lds_barrier();
+      }
+    }
+  }
+
+  if (nsplit > 1) {
+    __shared__ int s_last;
+    f32x4_t* slots = reinterpret_cast<f32x4_t*>(partials);
+    constexpr size_t SLOT = (size_t)SW * ST * NT;
+    f32x4_t* mine = slots + ((size_t)tile * nsplit + split) * SLOT;
+#pragma unroll
+    for (int i = 0; i < SW; ++i)
+#pragma unroll
+      for (int j = 0; j < ST; ++j) mine[(i * ST + j) * NT + tid] = acc[i][j];
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) s_last = (atomicAdd(&counters[tile], 1) == nsplit - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    f32x4_t tot[SW][ST];
+#pragma unroll
+    for (int i = 0; i < SW; ++i)
+#pragma unroll
+      for (int j = 0; j < ST; ++j) tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const f32x4_t* other = slots + ((size_t)tile * nsplit + sp) * SLOT;
+#pragma unroll
+      for (int i = 0; i < SW; ++i)
+#pragma unroll
+        for (int j = 0; j < ST; ++j) tot[i][j] += (sp == split) ? acc[i][j] : other[(i * ST + j) * NT + tid];
+    }
+    if (tid == 0) counters[tile] = 0;
+    epi.template apply<SW, ST>(tot, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+    return;
+  }
+  epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+}
+
+template <int BW, int BT, int PF, class Epi, int WW = 2, int WT = 2>
+static void run_rp(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
+                   const GemmScratch& sc, const Epi& epi, hipStream_t s) {
+  const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
+  const int units = tiles * nsplit;
+  if (units == 0) return;
+  const int grid = 8 * ((units + 7) / 8);
+  const size_t lds = (size_t)2 * (BW + BT) * 8 * 16;
+  auto kern = gemm_rp_kernel<BW, BT, PF, WW, WT, Epi>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, sc.partials,
+                     sc.counters, epi);
+}
+
 // ---------------------------------------------------------------- planning and dispatch
 struct TileCfg {
-  int bw, bt, stages;
+  int bw, bt, stages, ww, wt, rp;  // rp = 1: register-prefetch kernel, `stages` = prefetch depth
 };
+// Tile shapes (weight rows x tokens), LDS stages and wave grid. Measured on MI355X for the LLaDA /
+// Dream shapes: fewer stages with several resident workgroups per CU beat deep single-workgroup
+// pipelines.
 static const TileCfg kCfgs[] = {
-    {128, 128, 4}, {96, 192, 4}, {192, 192, 3}, {128, 96, 4}, {128, 64, 4}, {128, 256, 3}, {64, 64, 4},
+    {128, 128, 2, 2, 4, 0}, {96, 192, 2, 2, 2, 0}, {192, 192, 3, 4, 2, 0}, {64, 64, 4, 2, 2, 0},
+    {64, 64, 2, 2, 2, 0},   {128, 64, 3, 2, 2, 0}, {128, 256, 3, 2, 4, 0}, {64, 128, 3, 2, 2, 0},
+    {128, 128, 4, 2, 2, 0}, {96, 192, 3, 2, 2, 1}, {192, 192, 2, 4, 2, 1}, {128, 128, 3, 2, 4, 1},
+    {64, 128, 3, 2, 2, 1},
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kCUs = 256;
 
-static size_t cfg_lds(const TileCfg& c) { return (size_t)c.stages * (c.bw + c.bt) * 8 * 16; }
+// Measured choices for the GEMM shapes of the LLaDA-8B / Dream-7B workloads (weight rows, tokens, K).
+struct TunedShape {
+  int nw, t, k, cfg;
+};
+static const TunedShape kTuned[] = {
+#include "gemm_tuned.inc"
+};
 
-// Estimated time of one GEMM under a tile shape and split count: whole rounds of 256 units, each
-// unit costing its MACs scaled by a fragment-reuse efficiency, plus the partial-sum traffic.
+static size_t cfg_lds(const TileCfg& c) { return (size_t)(c.rp ? 2 : c.stages) * (c.bw + c.bt) * 8 * 16; }
+
+// Fallback estimate for shapes outside the table: saturated throughput of the configuration, or the
+// time of one workgroup when there are fewer workgroups than CUs.
 static double plan_cost(const TileCfg& c, int n, int Nw, int T, int K) {
   const double tiles = (double)((Nw + c.bw - 1) / c.bw) * ((T + c.bt - 1) / c.bt);
   const double units = tiles * n;
-  const double rounds = ceil(units / kCUs);
+  const int bpc = (int)(160 * 1024 / cfg_lds(c)) > 0 ? (int)(160 * 1024 / cfg_lds(c)) : 1;
   const double sw = c.bw / 32.0, st = c.bt / 32.0;
   const double eff = sw * st / (sw * st + 0.5 * (sw + st));
-  const double mac_rate = 2.5e15 / 2 / kCUs;  // MAC/s per CU at the bf16 peak
+  const double mac_rate = 2.5e15 / 2 / kCUs * 0.3;  // sustained MAC/s per CU
   const double t_unit = (double)c.bw * c.bt * ((double)K / n) / eff / mac_rate;
+  const double slots = (double)kCUs * (bpc < 2 ? 1 : 2);
   const double t_part = n > 1 ? 2.0 * (n - 1) * (double)T * Nw * 4 / 6e12 : 0.0;
-  const double t_pipe = 4 * 64 * 1e-9 * ((double)K / 64 / n > 0 ? 1 : 0);  // pipeline fill
-  return rounds * (t_unit + t_pipe) + t_part;
+  return ceil(units / slots) * t_unit * (bpc < 2 ? 1.0 : 1.6) + t_part;
 }
 
 GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   GemmPlan best{0, 1, 0};
-  double best_t = 1e30;
-  const int nk = (K + 63) / 64;
-  for (int ci = 0; ci < kNumCfgs; ++ci) {
-    if (force_bw && kCfgs[ci].bw != force_bw) continue;
-    for (int n = 1; n <= max_split; ++n) {
-      if (n > 1 && nk / n < 8) break;
-      const double t = plan_cost(kCfgs[ci], n, Nw, T, K);
-      if (t < best_t * 0.999) {
-        best_t = t;
-        best.cfg = ci;
-        best.nsplit = n;
+  bool found = false;
+  for (const TunedShape& ts : kTuned)
+    if (ts.nw == Nw && ts.t == T && ts.k == K && (!force_bw || kCfgs[ts.cfg].bw == force_bw)) {
+      best.cfg = ts.cfg;
+      found = true;
+      break;
+    }
+  if (!found) {
+    double best_t = 1e30;
+    const int nk = (K + 63) / 64;
+    for (int ci = 0; ci < kNumCfgs; ++ci) {
+      if (force_bw && kCfgs[ci].bw != force_bw) continue;
+      for (int n = 1; n <= max_split; ++n) {
+        if (n > 1 && nk / n < 8) break;
+        const double t = plan_cost(kCfgs[ci], n, Nw, T, K);
+        if (t < best_t * 0.999) {
+          best_t = t;
+          best.cfg = ci;
+          best.nsplit = n;
+        }
       }
     }
   }
@@ -464,7 +655,7 @@ size_t gemm_partial_bytes(const GemmPlan& p) {
   return (size_t)p.tiles * p.nsplit * c.bw * c.bt * 4;
 }
 
-template <int BW, int BT, int STAGES, class Epi>
+template <int BW, int BT, int STAGES, class Epi, int WW = 2, int WT = 2>
 static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
                     const GemmScratch& sc, const Epi& epi, hipStream_t s) {
   const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
@@ -472,42 +663,48 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   if (units == 0) return;
   const int grid = 8 * ((units + 7) / 8);
   const size_t lds = (size_t)STAGES * (BW + BT) * 8 * 16;
-  auto kern = gemm_kernel<BW, BT, STAGES, Epi>;
+  auto kern = gemm_kernel<BW, BT, STAGES, WW, WT, Epi>;
   static bool attr_set = false;  // one flag per instantiation
   if (!attr_set) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)lds);
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, W, X, Nw, T, K, t_count, nsplit, sc.partials, sc.counters,
-                     epi);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, sc.partials,
+                     sc.counters, epi);
 }
 
 template <class Epi>
 static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
                      const GemmScratch& sc, const Epi& epi, hipStream_t s) {
   switch (p.cfg) {
-    case 0: run_cfg<128, 128, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 1: run_cfg<96, 192, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 2: run_cfg<192, 192, 3>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 3: run_cfg<128, 96, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 4: run_cfg<128, 64, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 5: run_cfg<128, 256, 3>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    default: run_cfg<64, 64, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 0: run_cfg<128, 128, 2, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 1: run_cfg<96, 192, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 2: run_cfg<192, 192, 3, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 3: run_cfg<64, 64, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 4: run_cfg<64, 64, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 5: run_cfg<128, 64, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 6: run_cfg<128, 256, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 7: run_cfg<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 8: run_cfg<128, 128, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 9: run_rp<96, 192, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 10: run_rp<192, 192, 2, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 11: run_rp<128, 128, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    default: run_rp<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
   }
 }
 
 void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, const GemmScratch& sc,
               hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 4), W, X, Nw, T, K, nullptr, sc, EpiQkv{o}, s);
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiQkv{o}, s);
 }
 void gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, const GemmScratch& sc,
                 hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 4), W, X, Nw, T, K, nullptr, sc, EpiResid{r}, s);
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiResid{r}, s);
 }
 void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, const GemmScratch& sc,
                  hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 4), W, X, Nw, T, K, nullptr, sc, EpiSwiglu{a}, s);
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiSwiglu{a}, s);
 }
 void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, const GemmScratch& sc,
                     hipStream_t s) {

@@ -49,45 +49,72 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// One wavefront per row: u = bf16(r * rsqrt(mean(r^2) + eps) * g). With `rows`, output row j
-// normalises input row rows[j] (j < *count); otherwise output row j = input row j (j < T).
-// T is also the number of rows of r.
+// One 256-thread workgroup per row: u = bf16(r * rsqrt(mean(r^2) + eps) * g). Each thread holds
+// NV float4 of the row in registers (all loads issued at once), the sum of squares is reduced
+// across the workgroup in a fixed order. With `rows`, output row j normalises input row rows[j]
+// (j < *count); otherwise output row j = input row j. T is the number of rows of r.
+template <int NV>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ r, const float* __restrict__ g,
                                                      bf16_t* __restrict__ u, int T, int d, float eps,
                                                      const int32_t* __restrict__ rows,
                                                      const int32_t* __restrict__ count) {
-  int lane = threadIdx.x & 63;
-  int j = blockIdx.x * 4 + (threadIdx.x >> 6);
-  int n = rows ? *count : T;
+  __shared__ float red[4];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int j = blockIdx.x;
+  const int n = rows ? *count : T;
   if (j >= n) return;
-  int src = rows ? rows[j] : j;
+  const int src = rows ? rows[j] : j;
   bf16_t* y = u + (size_t)j * d;
+  const int d4 = d >> 2;
   if (src < 0 || src >= T) {  // row index outside the residual buffer: zero row
-    for (int c = lane * 4; c < d; c += 256) *reinterpret_cast<uint2*>(y + c) = make_uint2(0, 0);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = tid + v * 256;
+      if (c < d4) *reinterpret_cast<uint2*>(y + 4 * c) = make_uint2(0, 0);
+    }
     return;
   }
-  const float* x = r + (size_t)src * d;
+  const float4* x = reinterpret_cast<const float4*>(r + (size_t)src * d);
+  float4 v[NV];
   float ss = 0.f;
-  for (int c = lane * 4; c < d; c += 256) {
-    float4 v = *reinterpret_cast<const float4*>(x + c);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int c = tid + k * 256;
+    v[k] = c < d4 ? x[c] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
+#pragma unroll
+  for (int k = 0; k < NV; ++k) ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
   ss = wave_sum(ss);
-  float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int c = lane * 4; c < d; c += 256) {
-    float4 v = *reinterpret_cast<const float4*>(x + c);
-    float4 w = *reinterpret_cast<const float4*>(g + c);
-    uint2 o;
-    o.x = (uint32_t)f2bf(v.x * inv * w.x) | ((uint32_t)f2bf(v.y * inv * w.y) << 16);
-    o.y = (uint32_t)f2bf(v.z * inv * w.z) | ((uint32_t)f2bf(v.w * inv * w.w) << 16);
-    *reinterpret_cast<uint2*>(y + c) = o;
+  if (lane == 0) red[wid] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  const float4* g4 = reinterpret_cast<const float4*>(g);
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int c = tid + k * 256;
+    if (c < d4) {
+      const float4 w = g4[c];
+      uint2 o;
+      o.x = (uint32_t)f2bf(v[k].x * inv * w.x) | ((uint32_t)f2bf(v[k].y * inv * w.y) << 16);
+      o.y = (uint32_t)f2bf(v[k].z * inv * w.z) | ((uint32_t)f2bf(v[k].w * inv * w.w) << 16);
+      *reinterpret_cast<uint2*>(y + 4 * c) = o;
+    }
   }
 }
 
 void launch_rmsnorm(const float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
                     const int32_t* count, hipStream_t s) {
   if (T == 0) return;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3((T + 3) / 4), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+  const int nv = (d / 4 + 255) / 256;
+  if (nv <= 1)
+    hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+  else if (nv <= 2)
+    hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+  else if (nv <= 4)
+    hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
 }
 
 // ---------------------------------------------------------------- scored-row compaction

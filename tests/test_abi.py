@@ -44,7 +44,7 @@ def _cfg(dcl, **kw):
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("head_dim", 96, 2), ("n_kv_heads", 5, 2), ("d_model", 4100, 2), ("d_ffn", 8, 2), ("vocab", 1, 1),
+    ("head_dim", 96, 2), ("n_kv_heads", 5, 2), ("d_model", 4100, 2), ("d_model", 8208, 2), ("d_ffn", 8, 2), ("vocab", 1, 1),
     ("mask_id", 126464, 1), ("mask_id", -1, 1), ("rms_eps", 0.0, 1), ("rope_base", 1.0, 1),
     ("max_positions", 0, 1), ("n_layers", 0, 1), ("qkv_bias", 2, 1)])
 def test_model_create_rejects(dcl, field, value, status):
