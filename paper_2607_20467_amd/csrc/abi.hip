@@ -111,19 +111,8 @@ StepLayout step_layout(const dcl_config& c, int B, int S) {
   L.pm2 = take(np);
   L.pi2 = take(np);
   L.ps = take(np);
-  // split-K scratch of the four per-layer GEMMs (their shapes are fixed by B*S)
-  const int Ti = (int)T, qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
-  const GemmPlan plans[4] = {plan_gemm(qkv, Ti, c.d_model, 0, 1), plan_gemm(c.d_model, Ti, c.n_heads * c.head_dim, 0, 1),
-                             plan_gemm(2 * c.d_ffn, Ti, c.d_model, 0, 1), plan_gemm(c.d_model, Ti, c.d_ffn, 0, 1)};
-  size_t part = 0;
-  int ntile = 1;
-  for (const GemmPlan& gp : plans) {
-    if (gemm_partial_bytes(gp) > part) part = gemm_partial_bytes(gp);
-    if (gp.nsplit > 1 && gp.tiles > ntile) ntile = gp.tiles;
-  }
-  L.gpart = take(part ? part : 16);
-  L.gcnt = take((size_t)ntile * 4);
-  L.n_cnt = ntile;
+  // K-split slices of the residual GEMMs, folded into r by the next RMSNorm
+  L.part = take((size_t)kMaxSplit * T * d * 4);
   L.total = off;
   return L;
 }
@@ -215,8 +204,9 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   return DCL_OK;
 }
 
-// a2-a7: embedding and every transformer layer; leaves the residual stream in ws.r.
-void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_kv* kv, void* ws,
+// a2-a7: embedding and every transformer layer. Returns the number of K-split slices of the last
+// residual GEMM still to be added to ws.r (the final RMSNorm folds them in).
+int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_kv* kv, void* ws,
                  const StepLayout& L, hipStream_t s) {
   const dcl_config& c = m->cfg;
   const int T = B * S, d = c.d_model, dh = c.head_dim;
@@ -226,16 +216,17 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
   bf16_t* u = at<bf16_t>(ws, L.u);
   bf16_t* a = at<bf16_t>(ws, L.a);
   bf16_t* o = at<bf16_t>(ws, L.o);
-  const GemmScratch sc{at<float>(ws, L.gpart), at<int32_t>(ws, L.gcnt)};
+  float* part = at<float>(ws, L.part);
+  int pending = 0;  // K-split slices of the last residual GEMM not yet added to r
   {
     PROF(P_EMBED);
-    launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, at<int32_t>(ws, L.gcnt), L.n_cnt, s);
+    launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, s);
   }
   for (int l = 0; l < c.n_layers; ++l) {
     const LayerOffsets& lo = m->lay.layer[l];
     {
       PROF(P_NORM);
-      launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, s);
+      launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, part, pending, s);
     }
     QkvOut qo;
     qo.q = at<bf16_t>(ws, L.q);
@@ -251,7 +242,7 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     qo.pos0 = P;
     {
       PROF(P_QKV);
-      gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, sc, s);
+      gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
     }
     AttnArgs aa;
     aa.q = qo.q;
@@ -274,21 +265,22 @@ void run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_
     }
     {
       PROF(P_O);
-      gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, sc, s);
+      pending = gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, part, s);
     }
     {
       PROF(P_NORM);
-      launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, s);
+      launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, part, pending, s);
     }
     {
       PROF(P_GU);
-      gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, sc, s);
+      gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
     }
     {
       PROF(P_DOWN);
-      gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, sc, s);
+      pending = gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, part, s);
     }
   }
+  return pending;
 }
 
 }  // namespace
@@ -436,7 +428,7 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   const dcl_config& c = m->cfg;
   const StepLayout L = step_layout(c, B, S);
   (void)hipGetLastError();  // clear a stale error so the check below reports this call's launches
-  run_forward(m, tokens, B, S, kv, ws, L, stream);
+  const int pending = run_forward(m, tokens, B, S, kv, ws, L, stream);
   int32_t* rows = at<int32_t>(ws, L.rows);
   int32_t* count = at<int32_t>(ws, L.count);
   hipStream_t s = stream;
@@ -449,7 +441,7 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   {
     PROF(P_NORM);
     launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count,
-                   stream);
+                   at<float>(ws, L.part), pending, stream);
   }
   LmOut lo;
   lo.pm1 = at<float>(ws, L.pm1);
@@ -461,8 +453,7 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   lo.count = count;
   {
     PROF(P_LM);
-    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, GemmScratch{nullptr, nullptr},
-                stream);
+    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
   }
   {
     PROF(P_MERGE);
@@ -540,7 +531,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   int32_t* rows = at<int32_t>(ws, L.rows);
   int32_t* count = at<int32_t>(ws, L.count);
   hipStream_t s = stream;
-  launch_iota(rows, count, n, nullptr, 0, stream);
+  launch_iota(rows, count, n, stream);
   LmOut lo;
   lo.pm1 = at<float>(ws, L.pm1);
   lo.pi1 = at<int32_t>(ws, L.pi1);
@@ -552,7 +543,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   {
     PROF(P_LM);
     gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), static_cast<const bf16_t*>(hidden), m->cfg.vocab, n, m->cfg.d_model,
-                lo, GemmScratch{nullptr, nullptr}, stream);
+                lo, stream);
   }
   {
     PROF(P_MERGE);
@@ -572,14 +563,14 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
   const dcl_config& c = m->cfg;
   const StepLayout L = step_layout(c, B, S);
   (void)hipGetLastError();
-  run_forward(m, tokens, B, S, kv, ws, L, stream);
+  const int pending = run_forward(m, tokens, B, S, kv, ws, L, stream);
   // the row count goes to the device through a kernel argument (no host buffer to keep alive)
   int32_t* count = at<int32_t>(ws, L.count);
-  launch_iota(at<int32_t>(ws, L.pm1), count, n_rows, nullptr, 0, stream);
+  launch_iota(at<int32_t>(ws, L.pm1), count, n_rows, stream);
   bf16_t* hf = at<bf16_t>(ws, L.hf);
-  launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count, stream);
-  gemm_store_f32(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, n_rows, c.d_model, out, GemmScratch{nullptr, nullptr},
-                 stream);
+  launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count,
+                 at<float>(ws, L.part), pending, stream);
+  gemm_store_f32(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, n_rows, c.d_model, out, stream);
   if (hidden_out) {
     st = hip_check(hipMemcpyAsync(hidden_out, hf, (size_t)n_rows * c.d_model * 2, hipMemcpyDeviceToDevice, stream),
                    "hipMemcpyAsync(hidden_out)");

@@ -40,24 +40,25 @@ struct Model {
 
 // Step workspace layout.
 struct StepLayout {
-  size_t r, u, q, k, vt, o, a, rows, count, hf, pm1, pi1, pm2, pi2, ps, gpart, gcnt, total;
-  int T, S, Sp, n_vt, n_cnt;
+  size_t r, u, q, k, vt, o, a, rows, count, hf, pm1, pi1, pm2, pi2, ps, part, total;
+  int T, S, Sp, n_vt;
 };
 
 // Vocabulary tile of the fused LM-head reduction (vocab ids per partial).
 constexpr int kLmTile = 128;
 
 // ---------------------------------------------------------------- launchers (stream-ordered)
-void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, int32_t* zero_cnt,
-                  int n_zero, hipStream_t s);
-void launch_rmsnorm(const float* r, const float* g, bf16_t* u, int T, int d, float eps,
-                    const int32_t* rows, const int32_t* count, hipStream_t s);
+void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, hipStream_t s);
+// u = bf16(rmsnorm(r) * g). With nP > 0, first r + P[0] + ... + P[nP-1] (slices [T, d]) in that
+// order, written back to r unless `rows` selects the rows (final norm).
+void launch_rmsnorm(float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
+                    const int32_t* count, const float* P, int nP, hipStream_t s);
 void launch_compact(const int32_t* tokens, const int32_t* p, int B, int S, int gen_end, int mask_id,
                     int score_all, int32_t* rows, int32_t* count, dcl_row_stats st, hipStream_t s);
 void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const int32_t* pi2,
                   const float* ps, int n_vt, const int32_t* rows, const int32_t* count, int max_rows,
                   dcl_row_stats st, hipStream_t s);
-void launch_iota(int32_t* rows, int32_t* count, int n, int32_t* zero_cnt, int n_zero, hipStream_t s);
+void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s);
 void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c,
                    float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
                    uint32_t flags, hipStream_t s);
@@ -79,29 +80,20 @@ struct LmOut {
   int n_vt;
   const int32_t* count;  // number of valid X rows (device)
 };
-// Tile shape / split-K choice for one GEMM shape (host); the same plan sizes the workspace.
+// Tile shape / split-K choice for one GEMM shape (host).
 struct GemmPlan {
   int cfg, nsplit, tiles;
 };
-// force_bw: restrict to tiles of that many weight rows (0: any); max_split: largest split-K factor.
+// force_bw: restrict to tiles of that many weight rows (0: any); max_split: largest K-split factor.
 GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split);
-size_t gemm_partial_bytes(const GemmPlan& p);
-// Split-K scratch: float32 partial tiles and one arrival counter per output tile (zero between GEMMs).
-struct GemmScratch {
-  float* partials;
-  int32_t* counters;
-};
-constexpr int kMaxGemmTiles = 65536;  // counter slots in a workspace
-void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, const GemmScratch& sc,
-              hipStream_t s);
-void gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, const GemmScratch& sc,
-                hipStream_t s);
-void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, const GemmScratch& sc,
-                 hipStream_t s);
-void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, const GemmScratch& sc,
-                 hipStream_t s);
-void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, const GemmScratch& sc,
-                    hipStream_t s);
+constexpr int kMaxSplit = 4;  // K-split slices of the residual GEMMs
+void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, hipStream_t s);
+// r += W X^T, either in place (returns 0) or as n float32 slices P[s][T][Nw] that the next RMSNorm
+// folds into r in split order (returns n > 1). P may be null (in place only).
+int gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, float* P, hipStream_t s);
+void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, hipStream_t s);
+void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, hipStream_t s);
+void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, hipStream_t s);
 
 // Non-causal attention over [cache (P keys) || fresh (S keys)].
 struct AttnArgs {

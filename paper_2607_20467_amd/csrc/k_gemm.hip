@@ -34,8 +34,9 @@ __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, 
 
 struct EpiResid {
   float* r;
+  static constexpr bool kPartial = false;
   template <int SW, int ST>
-  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int, int) const {
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -56,8 +57,9 @@ struct EpiResid {
 
 struct EpiSwiglu {
   bf16_t* a;  // [T, Nw/2]
+  static constexpr bool kPartial = false;
   template <int SW, int ST>
-  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int, int) const {
     const int F = Nw >> 1;
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
@@ -79,8 +81,9 @@ struct EpiSwiglu {
 
 struct EpiQkv {
   QkvOut o;
+  static constexpr bool kPartial = false;
   template <int SW, int ST>
-  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int, int) const {
     const int dh = o.dh, half = dh >> 1;
     const int qrows = o.H * dh, krows = o.Hkv * dh;
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
@@ -132,8 +135,9 @@ struct EpiQkv {
 
 struct EpiF32 {
   float* out;
+  static constexpr bool kPartial = false;
   template <int SW, int ST>
-  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int, int) const {
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -146,6 +150,32 @@ struct EpiF32 {
           const int w = wq + 16 * i + r;
           if (w < Nw) out[(size_t)t * Nw + w] = acc[i][j][r];
         }
+    }
+  }
+};
+
+// Split-K slice: unit `split` writes its float32 partial C to P + split * stride ([T, Nw] each);
+// the consumer (the next RMSNorm) adds the slices to the residual stream in split order.
+struct EpiPartial {
+  float* P;
+  size_t stride;
+  static constexpr bool kPartial = true;
+  template <int SW, int ST>
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int,
+                                        int split) const {
+    float* base = P + (size_t)split * stride;
+    const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
+#pragma unroll
+    for (int j = 0; j < ST; ++j) {
+      const int t = tl + 16 * j;
+      if (t >= T) continue;
+#pragma unroll
+      for (int i = 0; i < SW; ++i) {
+        const int w = wq + 16 * i;
+        if (w >= Nw) continue;
+        *reinterpret_cast<float4*>(base + (size_t)t * Nw + w) =
+            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
     }
   }
 };
@@ -186,8 +216,9 @@ __device__ __forceinline__ Part part_merge(const Part& a, const Part& b) {
 template <int BW, int WW>
 struct EpiLm {
   LmOut o;
+  static constexpr bool kPartial = false;
   template <int SW, int ST>
-  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int tile_w) const {
+  __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int tile_w, int) const {
     __shared__ Part xch[WW][256];  // [wave along W][token within the workgroup tile]; BT <= 256
     const int wid = threadIdx.x >> 6;
     const int wave_w = wid % WW, wave_t = wid / WW;
@@ -260,10 +291,10 @@ struct EpiLm {
 // stage k is computed; vmcnt waits count only this wave's own outstanding stages, and a bare
 // s_barrier (no vmcnt(0) fence) publishes the stage to the other waves.
 //
-// Split-K: unit (tile, split) accumulates K-steps [split*per, ...). With nsplit > 1 every unit
-// writes its float32 partial to the workspace and increments the tile's counter; the last unit to
-// arrive adds the partials in split order (fixed, so results are bitwise reproducible), resets the
-// counter and runs the epilogue. No unit waits on another.
+// Split-K: unit (tile, split) accumulates K-steps [split*per, ...) and hands its partial to a
+// slice epilogue (EpiPartial: one float32 slice per split, no unit waits on another); the consumer
+// adds the slices in split order, so results are bitwise reproducible. nsplit > 1 is only used with
+// a slice epilogue.
 __device__ __attribute__((aligned(64))) uint4 g_zero_chunk[4];
 
 template <int N>
@@ -277,8 +308,7 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 template <int BW, int BT, int STAGES, int WW, int WT, class Epi>
 __global__ void __launch_bounds__(WW * WT * 64)
 gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
-            const int32_t* __restrict__ t_count, int nsplit, float* __restrict__ partials,
-            int32_t* __restrict__ counters, Epi epi) {
+            const int32_t* __restrict__ t_count, int nsplit, Epi epi) {
   constexpr int NWAVE = WW * WT, NT = NWAVE * 64;
   constexpr int TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
   constexpr int CH = (BW + BT) * 8;     // 16-byte chunks per stage
@@ -380,49 +410,21 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
     }
   }
 
-  if (nsplit > 1) {
-    __shared__ int s_last;
-    f32x4_t* slots = reinterpret_cast<f32x4_t*>(partials);
-    constexpr size_t SLOT = (size_t)SW * ST * NT;  // float4 per unit
-    f32x4_t* mine = slots + ((size_t)tile * nsplit + split) * SLOT;
-#pragma unroll
-    for (int i = 0; i < SW; ++i)
-#pragma unroll
-      for (int j = 0; j < ST; ++j) mine[(i * ST + j) * NT + tid] = acc[i][j];
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&counters[tile], 1) == nsplit - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    f32x4_t tot[SW][ST];
-#pragma unroll
-    for (int i = 0; i < SW; ++i)
-#pragma unroll
-      for (int j = 0; j < ST; ++j) tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const f32x4_t* other = slots + ((size_t)tile * nsplit + sp) * SLOT;
-#pragma unroll
-      for (int i = 0; i < SW; ++i)
-#pragma unroll
-        for (int j = 0; j < ST; ++j) tot[i][j] += (sp == split) ? acc[i][j] : other[(i * ST + j) * NT + tid];
-    }
-    if (tid == 0) counters[tile] = 0;  // ready for the next launch
-    epi.template apply<SW, ST>(tot, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+  if constexpr (Epi::kPartial) {
+    epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
     return;
   }
-  epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+  epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
 }
 
 // Register-prefetch variant: global -> VGPR loads run PF stages ahead of the MFMAs (the data in
 // flight sits in registers, not in LDS), each stage is written into a double-buffered,
 // XOR-swizzled LDS tile just before it is needed. The compiler's vmcnt waits cover exactly the
-// stage being stored. Same unit order, split-K and epilogues as gemm_kernel.
+// stage being stored. Same unit order, split-K slices and epilogues as gemm_kernel.
 template <int BW, int BT, int PF, int WW, int WT, class Epi>
 __global__ void __launch_bounds__(WW * WT * 64)
 gemm_rp_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
-               const int32_t* __restrict__ t_count, int nsplit, float* __restrict__ partials,
-               int32_t* __restrict__ counters, Epi epi) {
+               const int32_t* __restrict__ t_count, int nsplit, Epi epi) {
   constexpr int NWAVE = WW * WT, NT = NWAVE * 64;
   constexpr int TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
   constexpr int CH = (BW + BT) * 8;   // 16-byte chunks per stage
@@ -525,43 +527,16 @@ gemm_rp_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int N
     }
   }
 
-  if (nsplit > 1) {
-    __shared__ int s_last;
-    f32x4_t* slots = reinterpret_cast<f32x4_t*>(partials);
-    constexpr size_t SLOT = (size_t)SW * ST * NT;
-    f32x4_t* mine = slots + ((size_t)tile * nsplit + split) * SLOT;
-#pragma unroll
-    for (int i = 0; i < SW; ++i)
-#pragma unroll
-      for (int j = 0; j < ST; ++j) mine[(i * ST + j) * NT + tid] = acc[i][j];
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&counters[tile], 1) == nsplit - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    f32x4_t tot[SW][ST];
-#pragma unroll
-    for (int i = 0; i < SW; ++i)
-#pragma unroll
-      for (int j = 0; j < ST; ++j) tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const f32x4_t* other = slots + ((size_t)tile * nsplit + sp) * SLOT;
-#pragma unroll
-      for (int i = 0; i < SW; ++i)
-#pragma unroll
-        for (int j = 0; j < ST; ++j) tot[i][j] += (sp == split) ? acc[i][j] : other[(i * ST + j) * NT + tid];
-    }
-    if (tid == 0) counters[tile] = 0;
-    epi.template apply<SW, ST>(tot, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+  if constexpr (Epi::kPartial) {
+    epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
     return;
   }
-  epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w);
+  epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
 }
 
 template <int BW, int BT, int PF, class Epi, int WW = 2, int WT = 2>
 static void run_rp(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
-                   const GemmScratch& sc, const Epi& epi, hipStream_t s) {
+                   const Epi& epi, hipStream_t s) {
   const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
   const int units = tiles * nsplit;
   if (units == 0) return;
@@ -574,8 +549,7 @@ static void run_rp(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const
                               (int)lds);
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, sc.partials,
-                     sc.counters, epi);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, epi);
 }
 
 // ---------------------------------------------------------------- planning and dispatch
@@ -596,7 +570,7 @@ constexpr int kCUs = 256;
 
 // Measured choices for the GEMM shapes of the LLaDA-8B / Dream-7B workloads (weight rows, tokens, K).
 struct TunedShape {
-  int nw, t, k, cfg;
+  int nw, t, k, cfg, nsplit;
 };
 static const TunedShape kTuned[] = {
 #include "gemm_tuned.inc"
@@ -623,8 +597,10 @@ GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   GemmPlan best{0, 1, 0};
   bool found = false;
   for (const TunedShape& ts : kTuned)
-    if (ts.nw == Nw && ts.t == T && ts.k == K && (!force_bw || kCfgs[ts.cfg].bw == force_bw)) {
+    if (ts.nw == Nw && ts.t == T && ts.k == K && ts.nsplit <= max_split &&
+        (!force_bw || kCfgs[ts.cfg].bw == force_bw)) {
       best.cfg = ts.cfg;
+      best.nsplit = ts.nsplit;
       found = true;
       break;
     }
@@ -649,15 +625,9 @@ GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   return best;
 }
 
-size_t gemm_partial_bytes(const GemmPlan& p) {
-  if (p.nsplit <= 1) return 0;
-  const TileCfg& c = kCfgs[p.cfg];
-  return (size_t)p.tiles * p.nsplit * c.bw * c.bt * 4;
-}
-
 template <int BW, int BT, int STAGES, class Epi, int WW = 2, int WT = 2>
 static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
-                    const GemmScratch& sc, const Epi& epi, hipStream_t s) {
+                    const Epi& epi, hipStream_t s) {
   const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
   const int units = tiles * nsplit;
   if (units == 0) return;
@@ -670,50 +640,50 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
                               (int)lds);
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, sc.partials,
-                     sc.counters, epi);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, epi);
 }
 
 template <class Epi>
 static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
-                     const GemmScratch& sc, const Epi& epi, hipStream_t s) {
+                     const Epi& epi, hipStream_t s) {
   switch (p.cfg) {
-    case 0: run_cfg<128, 128, 2, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 1: run_cfg<96, 192, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 2: run_cfg<192, 192, 3, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 3: run_cfg<64, 64, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 4: run_cfg<64, 64, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 5: run_cfg<128, 64, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 6: run_cfg<128, 256, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 7: run_cfg<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 8: run_cfg<128, 128, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 9: run_rp<96, 192, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 10: run_rp<192, 192, 2, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    case 11: run_rp<128, 128, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
-    default: run_rp<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, sc, epi, s); break;
+    case 0: run_cfg<128, 128, 2, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 1: run_cfg<96, 192, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 2: run_cfg<192, 192, 3, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 3: run_cfg<64, 64, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 4: run_cfg<64, 64, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 5: run_cfg<128, 64, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 6: run_cfg<128, 256, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 7: run_cfg<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 8: run_cfg<128, 128, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 9: run_rp<96, 192, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 10: run_rp<192, 192, 2, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 11: run_rp<128, 128, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    default: run_rp<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
   }
 }
 
-void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, const GemmScratch& sc,
-              hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiQkv{o}, s);
+void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, EpiQkv{o}, s);
 }
-void gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, const GemmScratch& sc,
-                hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiResid{r}, s);
+int gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, float* P, hipStream_t s) {
+  const GemmPlan p = plan_gemm(Nw, T, K, 0, P ? kMaxSplit : 1);
+  if (p.nsplit > 1) {
+    run_plan(p, W, X, Nw, T, K, nullptr, EpiPartial{P, (size_t)T * Nw}, s);
+    return p.nsplit;
+  }
+  run_plan(p, W, X, Nw, T, K, nullptr, EpiResid{r}, s);
+  return 0;
 }
-void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, const GemmScratch& sc,
-                 hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiSwiglu{a}, s);
+void gemm_swiglu(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, bf16_t* a, hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, EpiSwiglu{a}, s);
 }
-void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, const GemmScratch& sc,
-                    hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, sc, EpiF32{out}, s);
+void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* out, hipStream_t s) {
+  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, EpiF32{out}, s);
 }
-void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, const GemmScratch& sc,
-                 hipStream_t s) {
+void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, hipStream_t s) {
   static_assert(kLmTile == 128, "the LM-head vocabulary tile is the GEMM's weight tile");
-  run_plan(plan_gemm(V, T, K, kLmTile, 1), W, X, V, T, K, o.count, sc, EpiLm<128, 2>{o}, s);
+  run_plan(plan_gemm(V, T, K, kLmTile, 1), W, X, V, T, K, o.count, EpiLm<128, 2>{o}, s);
 }
 
 }  // namespace dcl

@@ -9,14 +9,11 @@ namespace dcl {
 
 // ---------------------------------------------------------------- embedding gather
 // r[t, :] = E[tokens[t], :] widened to float32; ids outside [0, V) give a zero row.
-// The first n_zero threads also clear the split-K arrival counters of the step's GEMMs.
 __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ tokens,
                                                    const bf16_t* __restrict__ E, float* __restrict__ r,
-                                                   int T, int d, int V, int32_t* __restrict__ zero_cnt,
-                                                   int n_zero) {
+                                                   int T, int d, int V) {
   const int chunks = d / 8;
   long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < n_zero) zero_cnt[idx] = 0;
   if (idx >= (long)T * chunks) return;
   int t = (int)(idx / chunks), c = (int)(idx % chunks);
   int id = tokens[t];
@@ -33,13 +30,10 @@ __global__ void __launch_bounds__(256) embed_kernel(const int32_t* __restrict__ 
   dst[1] = hi;
 }
 
-void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, int32_t* zero_cnt,
-                  int n_zero, hipStream_t s) {
+void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, hipStream_t s) {
   long n = (long)T * (d / 8);
-  if (n < n_zero) n = n_zero;
   if (n == 0) return;
-  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tokens, E, r, T, d, V, zero_cnt,
-                     n_zero);
+  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tokens, E, r, T, d, V);
 }
 
 // ---------------------------------------------------------------- RMSNorm
@@ -53,11 +47,15 @@ __device__ __forceinline__ float wave_sum(float v) {
 // NV float4 of the row in registers (all loads issued at once), the sum of squares is reduced
 // across the workgroup in a fixed order. With `rows`, output row j normalises input row rows[j]
 // (j < *count); otherwise output row j = input row j. T is the number of rows of r.
+// With nP > 0 the row first takes the K-split slices of the residual GEMM that produced it:
+// r + P[0] + ... + P[nP-1] (each [T, d], added in that order); without `rows` the sum is written
+// back to r (with `rows`, the final norm, r is not needed afterwards and stays as it is).
 template <int NV>
-__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ r, const float* __restrict__ g,
+__global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ r, const float* __restrict__ g,
                                                      bf16_t* __restrict__ u, int T, int d, float eps,
                                                      const int32_t* __restrict__ rows,
-                                                     const int32_t* __restrict__ count) {
+                                                     const int32_t* __restrict__ count,
+                                                     const float* __restrict__ P, int nP) {
   __shared__ float red[4];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int j = blockIdx.x;
@@ -74,13 +72,33 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
     }
     return;
   }
-  const float4* x = reinterpret_cast<const float4*>(r + (size_t)src * d);
+  float4* x = reinterpret_cast<float4*>(r + (size_t)src * d);
   float4 v[NV];
   float ss = 0.f;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const int c = tid + k * 256;
     v[k] = c < d4 ? x[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (nP > 0) {
+    for (int sp = 0; sp < nP; ++sp) {
+      const float4* ps = reinterpret_cast<const float4*>(P + ((size_t)sp * T + src) * d);
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        const int c = tid + k * 256;
+        if (c < d4) {
+          const float4 q = ps[c];
+          v[k].x += q.x; v[k].y += q.y; v[k].z += q.z; v[k].w += q.w;
+        }
+      }
+    }
+    if (!rows) {
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        const int c = tid + k * 256;
+        if (c < d4) x[c] = v[k];
+      }
+    }
   }
 #pragma unroll
   for (int k = 0; k < NV; ++k) ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
@@ -103,18 +121,18 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
-void launch_rmsnorm(const float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
-                    const int32_t* count, hipStream_t s) {
+void launch_rmsnorm(float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
+                    const int32_t* count, const float* P, int nP, hipStream_t s) {
   if (T == 0) return;
   const int nv = (d / 4 + 255) / 256;
   if (nv <= 1)
-    hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+    hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
   else if (nv <= 2)
-    hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+    hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
   else if (nv <= 4)
-    hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+    hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count);
+    hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
 }
 
 // ---------------------------------------------------------------- scored-row compaction
@@ -236,17 +254,14 @@ void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const 
 }
 
 // rows[j] = j for j < n, count = n (row map of dcl_score_hidden and dcl_debug_logits' copy).
-__global__ void iota_kernel(int32_t* __restrict__ rows, int32_t* __restrict__ count, int n,
-                            int32_t* __restrict__ zero_cnt, int n_zero) {
+__global__ void iota_kernel(int32_t* __restrict__ rows, int32_t* __restrict__ count, int n) {
   int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j < n) rows[j] = j;
   if (j == 0) *count = n;
-  if (j < n_zero) zero_cnt[j] = 0;
 }
 
-void launch_iota(int32_t* rows, int32_t* count, int n, int32_t* zero_cnt, int n_zero, hipStream_t s) {
-  const int m = n > n_zero ? n : n_zero;
-  hipLaunchKernelGGL(iota_kernel, dim3((m + 255) / 256), dim3(256), 0, s, rows, count, n, zero_cnt, n_zero);
+void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s) {
+  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, rows, count, n);
 }
 
 // ---------------------------------------------------------------- DCV + drafts + remask

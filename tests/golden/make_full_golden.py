@@ -1,0 +1,80 @@
+"""Write the expected step statistics of the full-size workloads (c2-c5) with the float64 oracle.
+
+Calls only ``oracle`` and ``synth``. For every workload it stores, per scored row, the oracle's
+top1 / top2 / conf / p2 / lse, the drift of the same definition evaluated in float32 (which sizes
+the whole-step tolerance), the oracle's selection on its own statistics, and checksums of a few
+weight tensors so a machine that regenerates different weights is detected.
+
+    python tests/golden/make_full_golden.py [c2 c3 c4 c5]     (about 10 minutes on 8 cores)
+"""
+import hashlib
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
+
+import oracle  # noqa: E402
+import synth  # noqa: E402
+from oracle.numerics import WeightView  # noqa: E402
+
+CHECK_TENSORS = ("embed", "l0.wq", "l0.wd", "lm_head")
+
+
+def checksums(stored):
+    return {n: hashlib.sha256(np.ascontiguousarray(stored[n]).tobytes()).hexdigest()[:16] for n in CHECK_TENSORS}
+
+
+def run(key, stored):
+    w = synth.WORKLOADS[key]
+    g = w.geom
+    tok, p = synth.initial_state(w)
+    kv = None
+    if w.kv_prefix:
+        caches = [synth.kv_cache_layer(w, l) for l in range(g.n_layers)]
+
+        def kv(b, l):
+            k, v = caches[l]
+            return synth.bf16_bits_to_f32(k[b]), synth.bf16_bits_to_f32(v[b])
+        kv.prefix = w.kv_prefix
+    W = WeightView(stored)
+    t0 = time.time()
+    ref = oracle.step(g, W, tok, p, w.gen_end, kv=kv)
+    t1 = time.time()
+    f32 = oracle.step(g, W, tok, p, w.gen_end, kv=kv, dtype=np.float32)
+    t2 = time.time()
+    m = ref["conf"] >= 0
+    rows = np.nonzero(m.reshape(-1))[0]
+    x, pn, kr, ke = oracle.select_contiguous(tok, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id,
+                                             ref["top1"], ref["conf"])
+    out = dict(tokens=tok, p=p, rows=rows.astype(np.int64),
+               top1=ref["top1"].reshape(-1)[rows], top2=ref["top2"].reshape(-1)[rows],
+               conf=ref["conf"].reshape(-1)[rows], p2=ref["p2"].reshape(-1)[rows], lse=ref["lse"].reshape(-1)[rows],
+               drift_conf=np.float64(np.abs(f32["conf"][m] - ref["conf"][m]).max()),
+               drift_lse=np.float64(np.abs(f32["lse"][m] - ref["lse"][m]).max()),
+               f32_top1_flips=np.int64((f32["top1"][m] != ref["top1"][m]).sum()),
+               sel_tokens=x, sel_p=pn, sel_k_raw=kr, sel_k_eff=ke,
+               checksum_names=np.array(CHECK_TENSORS), checksum_values=np.array([checksums(stored)[n] for n in CHECK_TENSORS]),
+               oracle_seconds=np.float64(t1 - t0))
+    np.savez_compressed(os.path.join(HERE, f"full_{key}.npz"), **out)
+    print(f"{key}: {len(rows)} scored rows, oracle {t1 - t0:.0f} s, float32 evaluation {t2 - t1:.0f} s, "
+          f"drift conf {out['drift_conf']:.3g} lse {out['drift_lse']:.3g}, K_eff {ke.tolist()}", flush=True)
+
+
+def main(keys):
+    cache = {}
+    for key in keys:
+        g = synth.WORKLOADS[key].geom
+        if g.name not in cache:
+            cache.clear()
+            t = time.time()
+            cache[g.name] = synth.make_weights(g)
+            print(f"generated {g.name} in {time.time() - t:.0f} s", flush=True)
+        run(key, cache[g.name])
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:] or ["c2", "c3", "c5", "c4"])
