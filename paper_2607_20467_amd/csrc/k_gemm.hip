@@ -317,19 +317,19 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
   static_assert(STAGES >= 2 && IPW * (STAGES - 2) < 64, "pipeline depth");
   extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
 
-  const int nW = (Nw + BW - 1) / BW, nTt = (T + BT - 1) / BT;
-  const int tiles = nW * nTt, units = tiles * nsplit;
+  // Units: (weight tile, split, token tile), token tile innermost so neighbours share a weight
+  // slice. Only token tiles holding valid rows (t_count, when given) are units. XCD x
+  // (= blockIdx % 8) walks a contiguous run of units, its workgroups striding through the run.
+  const int Tv = t_count ? min(T, *t_count) : T;
+  const int nW = (Nw + BW - 1) / BW, nTt = (Tv + BT - 1) / BT;
+  const int units = nW * nsplit * nTt;
   const int per = (units + 7) / 8;
-  const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
-  if (L >= units) return;
-  // unit order: weight tile, then split, then token tile (neighbours share a weight slice)
+  const int xcd = blockIdx.x & 7, stride = gridDim.x >> 3;
+  const int run_end = min(units, (xcd + 1) * per);
+  for (int L = xcd * per + (blockIdx.x >> 3); L < run_end; L += stride) {
   const int tile_t = L % nTt, rest = L / nTt;
   const int split = rest % nsplit, tile_w = rest / nsplit;
-  const int tile = tile_w * nTt + tile_t;
   const int w0 = tile_w * BW, t0 = tile_t * BT;
-  const int Tv = t_count ? min(T, *t_count) : T;
-  if (t0 >= Tv) return;  // every split of this tile leaves here: the tile is never finalised
-
   const int nk_all = (K + 63) / 64;
   const int kper = (nk_all + nsplit - 1) / nsplit;
   const int kb = min(nk_all, split * kper);
@@ -410,11 +410,9 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
     }
   }
 
-  if constexpr (Epi::kPartial) {
-    epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
-    return;
-  }
   epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
+  lds_barrier();  // the next unit's prologue overwrites LDS the epilogue may still read
+  }
 }
 
 // Register-prefetch variant: global -> VGPR loads run PF stages ahead of the MFMAs (the data in
@@ -631,7 +629,10 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
   const int units = tiles * nsplit;
   if (units == 0) return;
-  const int grid = 8 * ((units + 7) / 8);
+  // One workgroup per unit; with a device-side row count the grid is capped (workgroups stride
+  // over the units that turn out to be active) so inactive token tiles cost no dispatch.
+  int grid = 8 * ((units + 7) / 8);
+  if (t_count && grid > 8 * kCUs) grid = 8 * kCUs;
   const size_t lds = (size_t)STAGES * (BW + BT) * 8 * 16;
   auto kern = gemm_kernel<BW, BT, STAGES, WW, WT, Epi>;
   static bool attr_set = false;  // one flag per instantiation

@@ -56,6 +56,8 @@ def run(key, stored):
                drift_conf=np.float64(np.abs(f32["conf"][m] - ref["conf"][m]).max()),
                drift_lse=np.float64(np.abs(f32["lse"][m] - ref["lse"][m]).max()),
                f32_top1_flips=np.int64((f32["top1"][m] != ref["top1"][m]).sum()),
+               f32_conf=f32["conf"].reshape(-1)[rows], f32_lse=f32["lse"].reshape(-1)[rows],
+               f32_top1=f32["top1"].reshape(-1)[rows],
                sel_tokens=x, sel_p=pn, sel_k_raw=kr, sel_k_eff=ke,
                checksum_names=np.array(CHECK_TENSORS), checksum_values=np.array([checksums(stored)[n] for n in CHECK_TENSORS]),
                oracle_seconds=np.float64(t1 - t0))

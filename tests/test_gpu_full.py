@@ -1,0 +1,119 @@
+"""Full-size parity: the four 7-8B workloads (c2-c5) in the launch configuration bench.py times,
+against float64 oracle statistics stored by ``tests/golden/make_full_golden.py``.
+
+At 28-32 random-init layers the bf16 storage points amplify float32 rounding noise (see
+helpers.py), so the stored float32 evaluation of the oracle's own definition sizes the bar:
+the GPU's confidence / log-sum-exp differences from the float64 oracle must stay within
+DRIFT_FACTOR times that evaluation's differences, both in the maximum and in the median (the median
+is the sharper check: most rows are far from any rounding flip). Token ids may differ only where the
+oracle's top-1/top-2 logit gap is below the logit tolerance. Selections are bit-exact given the GPU
+statistics, and the acceptance length K equals the oracle's unless a window row lies within the
+confidence tolerance of the threshold.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+from helpers import CONF_TOL, DRIFT_FACTOR, LOGIT_TOL, runner_for, stats_to_np, to_dev
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+_runners = {}
+
+
+def _golden(key):
+    path = os.path.join(GOLDEN, f"full_{key}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"{path} not generated (tests/golden/make_full_golden.py)")
+    return np.load(path, allow_pickle=False)
+
+
+def _runner(w, gold):
+    import hashlib
+    import torch
+    name = w.geom.name
+    if name not in _runners:
+        _runners.clear()
+        torch.cuda.empty_cache()
+        stored = synth.make_weights(w.geom)
+        for n, h in zip(gold["checksum_names"], gold["checksum_values"]):
+            got = hashlib.sha256(np.ascontiguousarray(stored[str(n)]).tobytes()).hexdigest()[:16]
+            assert got == str(h), f"regenerated weight {n} differs from the one the golden values used"
+        _runners[name] = runner_for(w, stored)
+        del stored
+    return _runners[name]
+
+
+@pytest.mark.parametrize("key", ["c2", "c3", "c5", "c4"])
+def test_full_size_step(key):
+    import torch
+    import paper_2607_20467_amd as dcl
+    gold = _golden(key)
+    w = synth.WORKLOADS[key]
+    g = w.geom
+    print(f"case {key}: {w.description}", flush=True)
+    run = _runner(w, gold)
+    tok, p = gold["tokens"], gold["p"]
+    B, S = tok.shape
+    kv = None
+    if w.kv_prefix:
+        caches = [synth.kv_cache_layer(w, l) for l in range(g.n_layers)]
+        kv = ([torch.from_numpy(c[0].view(np.int16)).cuda() for c in caches],
+              [torch.from_numpy(c[1].view(np.int16)).cuda() for c in caches], w.kv_prefix)
+        del caches
+    t_dev, p_dev = to_dev(tok), to_dev(p)
+    st_dev = run.step(t_dev, p_dev, w.gen_end, kv=kv)
+    gpu = stats_to_np(st_dev)
+    rows = gold["rows"]
+    scored = np.zeros(B * S, bool)
+    scored[rows] = True
+    np.testing.assert_array_equal(gpu["conf"].reshape(-1) >= 0, scored, err_msg="scored-row sets differ")
+    gconf, glse, gtop = (gpu[k].reshape(-1)[rows] for k in ("conf", "lse", "top1"))
+    dconf = np.abs(gconf - gold["conf"])
+    dlse = np.abs(glse - gold["lse"])
+    fconf = np.abs(gold["f32_conf"] - gold["conf"])
+    flse = np.abs(gold["f32_lse"] - gold["lse"])
+    conf_tol = max(CONF_TOL, DRIFT_FACTOR * fconf.max())
+    logit_tol = max(LOGIT_TOL, DRIFT_FACTOR * flse.max())
+    gap = np.log(gold["conf"]) - np.log(gold["p2"])
+    tie = gap < logit_tol
+    mism = gtop != gold["top1"]
+    rep = dict(rows=len(rows), conf_max=float(dconf.max()), conf_median=float(np.median(dconf)),
+               f32_conf_max=float(fconf.max()), f32_conf_median=float(np.median(fconf)),
+               lse_max=float(dlse.max()), lse_median=float(np.median(dlse)),
+               f32_lse_max=float(flse.max()), f32_lse_median=float(np.median(flse)),
+               top1_mismatch=int(mism.sum()), f32_top1_flips=int(gold["f32_top1_flips"]),
+               near_tie_rows=int(tie.sum()), conf_tol=conf_tol, logit_tol=logit_tol)
+    print(key, rep, flush=True)
+    assert dconf.max() <= conf_tol and dlse.max() <= logit_tol
+    assert np.median(dconf) <= DRIFT_FACTOR * np.median(fconf) + 1e-6
+    assert np.median(dlse) <= DRIFT_FACTOR * np.median(flse) + 1e-6
+    assert not (mism & ~tie).any(), f"top1 differs outside near-tie rows: {np.nonzero(mism & ~tie)[0][:10]}"
+
+    # selection on the GPU statistics: bit-exact against the oracle's rule; K against the oracle's K
+    k_raw = torch.zeros(B, dtype=torch.int32, device="cuda")
+    k_eff = torch.zeros(B, dtype=torch.int32, device="cuda")
+    dcl.dcl_select_contiguous(t_dev, B, S, p_dev, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id, st_dev,
+                              k_raw, k_eff)
+    torch.cuda.synchronize()
+    x_ref, p_ref, kr_ref, ke_ref = oracle.select_contiguous(tok, p, w.gen_end, w.window, w.tau_commit, w.tau_draft,
+                                                            g.mask_id, gpu["top1"], gpu["conf"].astype(np.float64))
+    np.testing.assert_array_equal(t_dev.cpu().numpy(), x_ref)
+    np.testing.assert_array_equal(p_dev.cpu().numpy(), p_ref)
+    np.testing.assert_array_equal(k_raw.cpu().numpy(), kr_ref)
+    oracle_conf = np.full(B * S, -1.0)
+    oracle_conf[rows] = gold["conf"]
+    oracle_conf = oracle_conf.reshape(B, S)
+    for b in range(B):
+        pb = int(p[b])
+        win = oracle_conf[b, pb:pb + min(w.window, w.gen_end - pb)]
+        near = bool((np.abs(win - w.tau_commit) < conf_tol).any())
+        got_k = int(k_raw[b].item())
+        print(f"  seq {b}: K oracle {int(gold['sel_k_raw'][b])}, GPU {got_k}, near-threshold window: {near}", flush=True)
+        if not near:
+            assert got_k == int(gold["sel_k_raw"][b])
