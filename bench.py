@@ -43,6 +43,94 @@ def step_work(w, R):
     }
 
 
+def step_bytes(w, R):
+    """Algorithmic HBM bytes per launch of each kernel class: every operand read once, every result
+    written once (bf16 weights and activations, fp32 residual stream and split-K slices)."""
+    g = w.geom
+    T = w.batch * w.seq
+    P = w.kv_prefix
+    d, H, Hkv, dh, F, V = g.d_model, g.n_heads, g.n_kv_heads, g.head_dim, g.d_ffn, g.vocab
+    nq = (H + 2 * Hkv) * dh
+    return {
+        "gemm_qkv_rope": 2 * (nq * d + T * d + T * nq),
+        "attention": 2 * (T * H * dh + 2 * w.batch * Hkv * (w.seq + P) * dh + T * H * dh),
+        "gemm_o_residual": 2 * (d * H * dh + T * H * dh) + 4 * T * d,
+        "gemm_gate_up_swiglu": 2 * (2 * F * d + T * d + T * F),
+        "gemm_down_residual": 2 * (d * F + T * F) + 4 * T * d,
+        "gemm_lm_head_top2": 2 * (V * d + R * d),
+    }
+
+
+# Kernel sources whose change invalidates stored hardware-counter traffic figures.
+TRAFFIC_SOURCES = ["paper_2607_20467_amd/csrc/k_gemm.hip", "paper_2607_20467_amd/csrc/gemm_tuned.inc",
+                   "paper_2607_20467_amd/csrc/k_attn.hip", "paper_2607_20467_amd/csrc/dcl_internal.h",
+                   "paper_2607_20467_amd/csrc/abi.hip"]
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel_class, workload_key):
+    """HBM bytes per launch from a committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary, or None when
+    there is none or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload_key}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    rec = json.loads(text[start + 7:text.index("```", start + 7)])
+    if rec.get("source_digest") != kernel_source_digest():
+        log(f"traffic figures in {os.path.basename(path)} predate the current kernel sources: not used")
+        return None
+    return rec
+
+
+# rocprofv3 kernel names -> bench kernel classes (split-K slice GEMMs alternate o-proj, down-proj per layer)
+def kernel_class(name):
+    for key, cls in (("EpiSwiglu", "gemm_gate_up_swiglu"), ("EpiQkv", "gemm_qkv_rope"), ("EpiLm", "gemm_lm_head_top2"),
+                     ("attn_kernel", "attention"), ("rmsnorm_kernel", "rmsnorm"), ("embed_kernel", "embed"),
+                     ("compact_kernel", "compact"), ("merge_kernel", "merge"), ("select_kernel", "select"),
+                     ("copyBuffer", "copy"), ("pack_", "weight_packing")):
+        if key in name:
+            return cls
+    if "EpiPartial" in name or "EpiResid" in name:
+        return "gemm_o_or_down_residual"
+    return "other"
+
+
+def pmc_summary(csv_path, copy_mib):
+    """Per-kernel-class average of each counter in a rocprofv3 --pmc counter_collection.csv, with the
+    calibration factor from the largest plain copy (copy_mib MiB read and written once)."""
+    import collections
+    import csv
+    rows = list(csv.DictReader(open(csv_path)))
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    order = sorted({(int(r["Dispatch_Id"]), r["Kernel_Name"]) for r in rows})
+    split_seq = [d for d, n in order if kernel_class(n) == "gemm_o_or_down_residual"]
+    split_cls = {d: ("gemm_o_residual" if i % 2 == 0 else "gemm_down_residual") for i, d in enumerate(split_seq)}
+    for r in rows:
+        d = int(r["Dispatch_Id"])
+        cls = split_cls.get(d) or kernel_class(r["Kernel_Name"])
+        per[(cls, r["Counter_Name"])][d].append(float(r["Counter_Value"]))
+    out = {}
+    for (cls, ctr), disp in sorted(per.items()):
+        vals = [sum(v) for v in disp.values()]
+        out.setdefault(cls, {})[ctr] = {"dispatches": len(vals), "avg": sum(vals) / len(vals), "max": max(vals)}
+    if "copy" in out and copy_mib:
+        for ctr, ent in out["copy"].items():
+            kib = ent["max"]  # the calibration copy is the largest copyBuffer dispatch
+            ent["factor_bytes_per_unit"] = copy_mib * 1024 * 1024 / (kib * 1024.0) if kib else None
+    return out
+
+
 def step_flops(w, R):
     per = step_work(w, R)
     L = w.geom.n_layers
@@ -85,7 +173,15 @@ def main():
     ap.add_argument("--workload", default="c2", help="synth workload key (c2 = LLaDA-8B shape, B1, S384)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the event-timed kernel-class pass")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after timing, copy a buffer of this many MiB (hardware-counter calibration)")
+    ap.add_argument("--pmc-summary", metavar="CSV", help="summarise a rocprofv3 --pmc counter_collection.csv "
+                    "per kernel class and exit (with --copy-calibration-mib of the profiled run)")
     args = ap.parse_args()
+    if args.pmc_summary:
+        summ = pmc_summary(args.pmc_summary, args.copy_calibration_mib)
+        print(json.dumps({"source_digest": kernel_source_digest(), "classes": summ}, indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
               "one process drives one GPU", file=sys.stderr)
@@ -172,11 +268,28 @@ def main():
             classes[name] = ent
             log(f"  {name:22s} {n / args.steps:6.1f} launches/step  avg {avg_us:9.2f} us  "
                 f"{tms / args.steps:8.3f} ms/step" + (f"  {ent['tflops']:7.1f} TFLOP/s" if "tflops" in ent else ""))
+        alg_bytes = step_bytes(w, R)
+        for name, ent in classes.items():
+            if name in alg_bytes:
+                ent["gbs"] = round(alg_bytes[name] / (ent["avg_us"] * 1e-6) / 1e9, 1)
         dom = max((k for k in classes if k in per), key=lambda k: classes[k]["ms_per_step"])
         ach = per[dom] / (classes[dom]["avg_us"] * 1e-6) / 1e12
+        tr = stored_traffic(dom, w.key)
         roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None,
-                    "flop_per_launch": per[dom]}
+                    "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK_TFLOPS, 4),
+                    "traffic": tr["hbm_bytes_per_launch"] if tr else None,
+                    "flop_per_launch": per[dom], "algorithmic_bytes_per_launch": alg_bytes[dom],
+                    "avg_launch_us": classes[dom]["avg_us"]}
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * 1024 * 1024 // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {args.copy_calibration_mib} MiB three times (counter calibration)")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:
