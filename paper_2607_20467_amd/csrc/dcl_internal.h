@@ -44,8 +44,10 @@ struct StepLayout {
   int T, S, Sp, n_vt;
 };
 
-// Vocabulary tile of the fused LM-head reduction (vocab ids per partial).
+// Vocabulary tile of the fused LM-head reduction (vocab ids per partial) and the number of waves
+// that split it (their partials merge through LDS in the GEMM epilogue).
 constexpr int kLmTile = 128;
+constexpr int kLmWaves = 2;
 
 // ---------------------------------------------------------------- launchers (stream-ordered)
 void launch_embed(const int32_t* tokens, const bf16_t* E, float* r, int T, int d, int V, hipStream_t s);

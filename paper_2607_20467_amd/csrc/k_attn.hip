@@ -43,7 +43,14 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   static_assert(SCH % (64 * NW) == 0 && KCH % 64 == 0, "stage shape");
   extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
 
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  // Units (batch, head, query tile), query tile innermost: XCD x (= blockIdx % 8) takes a contiguous
+  // run of units, so the query tiles of one head (and the heads sharing a KV head) read their keys
+  // and values through one L2.
+  const int nqt = (a.S + BQ - 1) / BQ;
+  const int units = nqt * a.H * a.B, per = (units + 7) / 8;
+  const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  if (L >= units) return;
+  const int qt = L % nqt, h = (L / nqt) % a.H, b = L / (nqt * a.H);
   const int g = h / (a.H / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int lq = lane & 15, lg = lane >> 4;
@@ -194,7 +201,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
 
 template <int NW, int STAGES>
 static void run_attn(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.S + 16 * NW - 1) / (16 * NW), a.H, a.B);
+  const int units = ((a.S + 16 * NW - 1) / (16 * NW)) * a.H * a.B;
+  dim3 grid(8 * ((units + 7) / 8));
   const size_t lds = (size_t)STAGES * (KT * (a.dh / 8) + a.dh * (KT / 8)) * 16;
   if (a.dh == 128) {
     auto kern = attn_kernel<NW, 128, STAGES>;

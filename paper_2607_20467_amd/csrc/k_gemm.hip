@@ -284,12 +284,21 @@ struct EpiLm {
 };
 
 // ---------------------------------------------------------------- the kernel
-// Direct-to-LDS multi-stage pipeline: each stage holds a BW x 64 weight slice and a BT x 64
-// activation slice, written by global_load_lds_dwordx4 (16 bytes per lane straight into LDS, no
-// register staging). Rows are 8 chunks of 16 bytes, XOR-swizzled (chunk c of row r at c ^ (r & 7))
-// so the MFMA fragment reads are bank-conflict free. Loads for stage k + STAGES - 1 are issued while
-// stage k is computed; vmcnt waits count only this wave's own outstanding stages, and a bare
-// s_barrier (no vmcnt(0) fence) publishes the stage to the other waves.
+// Direct-to-LDS multi-stage pipeline: each stage holds a BW x KD weight slice and a BT x KD
+// activation slice (KD = 64 or 128 K elements), written by global_load_lds_dwordx4 (16 bytes per
+// lane straight into LDS, no register staging). A row is KD/8 chunks of 16 bytes, XOR-swizzled
+// (chunk c of row r at c ^ (r mod KD/8)) so the MFMA fragment reads are bank-conflict free.
+// All STAGES buffers are in flight at once: buffer k mod STAGES is refilled with stage
+// k + STAGES as soon as every wave holds stage k's fragments in registers. Fragments are double
+// buffered per 32-wide K substep: the LDS reads of substep s + 1 are in flight while the MFMAs of
+// substep s run, and the first substep of stage k + 1 is read across the stage boundary.
+//
+// The DMA instructions are issued from inline assembly (M0 = LDS destination of the wave), so
+// the compiler's wait-count pass does not treat them as pending LDS traffic and keeps its LDS
+// waits fine-grained; their completion is tracked here with vmcnt waits on this wave's own
+// outstanding stages, and a bare s_barrier (no vmcnt(0) fence) publishes a stage to the other
+// waves. Vector-memory loads complete in issue order, and no other vector-memory load is issued
+// inside the K loop, so "at most n outstanding" means "all but the newest n landed".
 //
 // Split-K: unit (tile, split) accumulates K-steps [split*per, ...) and hands its partial to a
 // slice epilogue (EpiPartial: one float32 slice per split, no unit waits on another); the consumer
@@ -305,113 +314,143 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int BW, int BT, int STAGES, int WW, int WT, class Epi>
+// One wave-wide 16-byte-per-lane copy global -> LDS; lane i lands at lds + 16 i.
+__device__ __forceinline__ void dma16(const void* g, const uint4* lds) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0v), "v"(g) : "memory", "m0");
+}
+
+template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi>
 __global__ void __launch_bounds__(WW * WT * 64)
 gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
             const int32_t* __restrict__ t_count, int nsplit, Epi epi) {
-  constexpr int NWAVE = WW * WT, NT = NWAVE * 64;
+  constexpr int NWAVE = WW * WT;
+  constexpr int CPR = KD / 8, KS = KD / 32;  // 16-byte chunks per row, 32-wide substeps per stage
   constexpr int TW = BW / WW, TT = BT / WT, SW = TW / 16, ST = TT / 16;
-  constexpr int CH = (BW + BT) * 8;     // 16-byte chunks per stage
-  constexpr int IPW = CH / 64 / NWAVE;  // load instructions per wave per stage
-  static_assert(TW % 16 == 0 && TT % 16 == 0 && CH % (64 * NWAVE) == 0 && (BW * 8) % 64 == 0, "tile shape");
-  static_assert(STAGES >= 2 && IPW * (STAGES - 2) < 64, "pipeline depth");
+  constexpr int CH = (BW + BT) * CPR;        // chunks per stage
+  constexpr int IPW = CH / 64 / NWAVE;       // load instructions per wave per stage
+  static_assert(TW % 16 == 0 && TT % 16 == 0 && CH % (64 * NWAVE) == 0 && (BW * CPR) % 64 == 0, "tile shape");
+  static_assert((KD == 64 || KD == 128) && STAGES >= 2 && IPW * (STAGES - 1) < 64, "pipeline shape");
   extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
 
-  // Units: (weight tile, split, token tile), token tile innermost so neighbours share a weight
-  // slice. Only token tiles holding valid rows (t_count, when given) are units. XCD x
-  // (= blockIdx % 8) walks a contiguous run of units, its workgroups striding through the run.
+  // Units: (split, weight tile, token tile), token tile innermost so neighbours share a weight
+  // slice, split outermost so an XCD's run covers one or two K ranges and its L2 holds only that
+  // part of the activations. Only token tiles holding valid rows (t_count, when given) are units.
+  // XCD x (= blockIdx % 8) walks a contiguous run of units, its workgroups striding through it.
   const int Tv = t_count ? min(T, *t_count) : T;
   const int nW = (Nw + BW - 1) / BW, nTt = (Tv + BT - 1) / BT;
   const int units = nW * nsplit * nTt;
   const int per = (units + 7) / 8;
   const int xcd = blockIdx.x & 7, stride = gridDim.x >> 3;
   const int run_end = min(units, (xcd + 1) * per);
-  for (int L = xcd * per + (blockIdx.x >> 3); L < run_end; L += stride) {
-  const int tile_t = L % nTt, rest = L / nTt;
-  const int split = rest % nsplit, tile_w = rest / nsplit;
-  const int w0 = tile_w * BW, t0 = tile_t * BT;
-  const int nk_all = (K + 63) / 64;
-  const int kper = (nk_all + nsplit - 1) / nsplit;
-  const int kb = min(nk_all, split * kper);
-  const int nk = min(nk_all, kb + kper) - kb;
-
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wave_w = wid % WW, wave_t = wid / WW;
+  const int frow = lane & 15, fchunk = lane >> 4;
+  for (int L = xcd * per + (blockIdx.x >> 3); L < run_end; L += stride) {
+    const int tile_t = L % nTt, rest = L / nTt;
+    const int tile_w = rest % nW, split = rest / nW;
+    const int w0 = tile_w * BW, t0 = tile_t * BT;
+    const int nk_all = (K + KD - 1) / KD;
+    const int kper = (nk_all + nsplit - 1) / nsplit;
+    const int kb = min(nk_all, split * kper);
+    const int nk = min(nk_all, kb + kper) - kb;
 
-  // Per-lane element offset of this wave's load instructions (loop invariant; -1 = row outside the
-  // operand). Instruction i of wave `wid` fills chunks [(wid*IPW + i)*64, +64) of the stage: all of
-  // them weight chunks or all activation chunks, so the operand choice is wave-uniform.
-  int off[IPW];
-#pragma unroll
-  for (int i = 0; i < IPW; ++i) {
-    const int q = wid * IPW + i;
-    const int pos = q * 64 + lane;
-    const bool isw = q * 64 < BW * 8;
-    const int p2 = isw ? pos : pos - BW * 8;
-    const int row = p2 >> 3, c = (p2 & 7) ^ (row & 7);
-    const int grow = (isw ? w0 : t0) + row;
-    off[i] = (grow < (isw ? Nw : Tv)) ? grow * K + c * 8 : -1;
-  }
-  const bool ktail = (K & 63) != 0;
-  auto issue = [&](int kt) {
-    uint4* stage = sm + (kt % STAGES) * CH;
-    const int k0 = (kb + kt) * 64;
+    // Per-lane element offset of this wave's load instructions (loop invariant; -1 = row outside
+    // the operand) and K offset of its chunk. Instruction i of wave `wid` fills chunks
+    // [(wid*IPW + i)*64, +64) of the stage: all weight chunks or all activation chunks.
+    int off[IPW], kc[IPW];
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const int q = wid * IPW + i;
-      const bf16_t* base = (q * 64 < BW * 8) ? W : X;
-      bool ok = off[i] >= 0;
-      if (ktail) {
-        const int p2 = (q * 64 < BW * 8 ? q * 64 : q * 64 - BW * 8) + lane;
-        ok = ok && k0 + ((p2 & 7) ^ ((p2 >> 3) & 7)) * 8 < K;
-      }
-      const void* g = ok ? static_cast<const void*>(base + (size_t)off[i] + k0) : static_cast<const void*>(g_zero_chunk);
-      __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(stage + q * 64), 16, 0, 0);
+      const int pos = q * 64 + lane;
+      const bool isw = q * 64 < BW * CPR;
+      const int p2 = isw ? pos : pos - BW * CPR;
+      const int row = p2 / CPR, c = (p2 % CPR) ^ (row & (CPR - 1));
+      const int grow = (isw ? w0 : t0) + row;
+      off[i] = (grow < (isw ? Nw : Tv)) ? grow * K + c * 8 : -1;
+      kc[i] = c * 8;
     }
-  };
-
-  f32x4_t acc[SW][ST];
+    const bool ktail = (K % KD) != 0;
+    auto issue = [&](int kt) {
+      const uint4* stage = sm + (kt % STAGES) * CH;
+      const int k0 = (kb + kt) * KD;
 #pragma unroll
-  for (int i = 0; i < SW; ++i)
-#pragma unroll
-    for (int j = 0; j < ST; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < nk) issue(st);
-  const int frow = lane & 15, fchunk = lane >> 4;
-  for (int kt = 0; kt < nk; ++kt) {
-    // stages issued but not yet needed after this one: min(STAGES - 2, nk - 1 - kt)
-    const int pending = min(STAGES - 2, nk - 1 - kt);
-    if (STAGES >= 4 && pending >= 2) wait_vmcnt<(STAGES >= 4 ? 2 : 0) * IPW>();
-    else if (pending >= 1) wait_vmcnt<IPW>();
-    else wait_vmcnt<0>();
-    lds_barrier();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
-    const uint4* stage = sm + (kt % STAGES) * CH;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+      for (int i = 0; i < IPW; ++i) {
+        const int q = wid * IPW + i;
+        const bf16_t* base = (q * 64 < BW * CPR) ? W : X;
+        const bool ok = off[i] >= 0 && (!ktail || k0 + kc[i] < K);
+        dma16(ok ? static_cast<const void*>(base + (size_t)off[i] + k0) : static_cast<const void*>(g_zero_chunk),
+              stage + q * 64);
+      }
+    };
+    auto frag = [&](int kt, int ks, bf16x8_t(&a)[SW], bf16x8_t(&b)[ST]) {
+      const uint4* stage = sm + (kt % STAGES) * CH;
       const int c = 4 * ks + fchunk;
-      bf16x8_t a[SW], b[ST];
 #pragma unroll
       for (int i = 0; i < SW; ++i) {
         const int r = wave_w * TW + 16 * i + frow;
-        a[i] = __builtin_bit_cast(bf16x8_t, stage[r * 8 + (c ^ (r & 7))]);
+        a[i] = __builtin_bit_cast(bf16x8_t, stage[r * CPR + (c ^ (r & (CPR - 1)))]);
       }
 #pragma unroll
       for (int j = 0; j < ST; ++j) {
         const int r = wave_t * TT + 16 * j + frow;
-        b[j] = __builtin_bit_cast(bf16x8_t, stage[BW * 8 + r * 8 + (c ^ (r & 7))]);
+        b[j] = __builtin_bit_cast(bf16x8_t, stage[BW * CPR + r * CPR + (c ^ (r & (CPR - 1)))]);
       }
+    };
+    f32x4_t acc[SW][ST];
+#pragma unroll
+    for (int i = 0; i < SW; ++i)
+#pragma unroll
+      for (int j = 0; j < ST; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    auto mma = [&](const bf16x8_t(&a)[SW], const bf16x8_t(&b)[ST]) {
 #pragma unroll
       for (int i = 0; i < SW; ++i)
 #pragma unroll
         for (int j = 0; j < ST; ++j) acc[i][j] = mfma16(a[i], b[j], acc[i][j]);
-    }
-  }
+    };
 
-  epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
-  lds_barrier();  // the next unit's prologue overwrites LDS the epilogue may still read
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st)
+      if (st < nk) issue(st);
+    {  // stage 0 landed; stages 1 .. min(nk, STAGES) - 1 may still fly
+      const int pend = min(STAGES - 1, nk - 1);
+      if (STAGES >= 3 && pend >= 2) wait_vmcnt<(STAGES >= 3 ? 2 : 0) * IPW>();
+      else if (pend >= 1) wait_vmcnt<IPW>();
+      else wait_vmcnt<0>();
+    }
+    lds_barrier();
+    bf16x8_t fa[2][SW], fb[2][ST];
+    if (nk > 0) frag(0, 0, fa[0], fb[0]);
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (s + 1 < KS) {
+          frag(kt, s + 1, fa[(s + 1) & 1], fb[(s + 1) & 1]);
+        } else {
+          // stage kt + 1 landed (stages kt + 2 .. min(nk - 1, kt + STAGES - 1) may still fly);
+          // after the barrier every wave holds stage kt in registers, so its buffer is refilled
+          const int pend = min(STAGES - 2, nk - 2 - kt);
+          if (STAGES >= 4 && pend >= 2) wait_vmcnt<(STAGES >= 4 ? 2 : 0) * IPW>();
+          else if (STAGES >= 3 && pend >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * IPW>();
+          else wait_vmcnt<0>();
+          lds_barrier();
+          if (kt + STAGES < nk) issue(kt + STAGES);
+          frag(kt + 1, 0, fa[0], fb[0]);
+        }
+        mma(fa[s & 1], fb[s & 1]);
+      }
+    }
+    if (nk > 0) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (s + 1 < KS) frag(nk - 1, s + 1, fa[(s + 1) & 1], fb[(s + 1) & 1]);
+        mma(fa[s & 1], fb[s & 1]);
+      }
+    }
+
+    epi.template apply<SW, ST>(acc, w0 + wave_w * TW, t0 + wave_t * TT, lane, Nw, Tv, tile_w, split);
+    lds_barrier();  // the next unit's prologue overwrites LDS the epilogue may still read
   }
 }
 
@@ -436,7 +475,7 @@ gemm_rp_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int N
   const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
   if (L >= units) return;
   const int tile_t = L % nTt, rest = L / nTt;
-  const int split = rest % nsplit, tile_w = rest / nsplit;
+  const int tile_w = rest % nW, split = rest / nW;
   const int tile = tile_w * nTt + tile_t;
   const int w0 = tile_w * BW, t0 = tile_t * BT;
   const int Tv = t_count ? min(T, *t_count) : T;
@@ -552,16 +591,20 @@ static void run_rp(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const
 
 // ---------------------------------------------------------------- planning and dispatch
 struct TileCfg {
-  int bw, bt, stages, ww, wt, rp;  // rp = 1: register-prefetch kernel, `stages` = prefetch depth
+  int bw, bt, kd, stages, ww, wt, rp;  // rp = 1: register-prefetch kernel, `stages` = prefetch depth
 };
-// Tile shapes (weight rows x tokens), LDS stages and wave grid. Measured on MI355X for the LLaDA /
-// Dream shapes: fewer stages with several resident workgroups per CU beat deep single-workgroup
-// pipelines.
+// Tile shapes (weight rows x tokens), K depth per stage, stages and wave grid, chosen among by
+// measurement on MI355X for the LLaDA / Dream shapes (the tuned table below). A K depth of 128
+// halves the number of stage handoffs, which is what limits the small-tile shapes; 8-16 waves per
+// workgroup keep the MFMA pipes busy while the LDS fragment reads of the next substep are in
+// flight.
 static const TileCfg kCfgs[] = {
-    {128, 128, 2, 2, 4, 0}, {96, 192, 2, 2, 2, 0}, {192, 192, 3, 4, 2, 0}, {64, 64, 4, 2, 2, 0},
-    {64, 64, 2, 2, 2, 0},   {128, 64, 3, 2, 2, 0}, {128, 256, 3, 2, 4, 0}, {64, 128, 3, 2, 2, 0},
-    {128, 128, 4, 2, 2, 0}, {96, 192, 3, 2, 2, 1}, {192, 192, 2, 4, 2, 1}, {128, 128, 3, 2, 4, 1},
-    {64, 128, 3, 2, 2, 1},
+    {128, 128, 64, 2, 2, 4, 0},  {192, 192, 64, 3, 4, 2, 0},  {64, 64, 64, 4, 2, 2, 0},
+    {128, 256, 64, 3, 2, 4, 0},  {96, 192, 64, 3, 2, 2, 1},   {192, 192, 64, 2, 4, 2, 1},
+    {128, 128, 64, 3, 2, 4, 1},  {96, 192, 128, 2, 3, 4, 0},  {128, 96, 128, 2, 4, 2, 0},
+    {160, 128, 128, 2, 2, 4, 0}, {96, 192, 128, 2, 2, 4, 0},  {192, 192, 64, 3, 4, 4, 0},
+    {128, 128, 128, 2, 2, 4, 0}, {64, 192, 128, 2, 2, 4, 0},  {128, 192, 128, 2, 4, 4, 0},
+    {128, 128, 64, 3, 2, 4, 0},
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kCUs = 256;
@@ -574,7 +617,9 @@ static const TunedShape kTuned[] = {
 #include "gemm_tuned.inc"
 };
 
-static size_t cfg_lds(const TileCfg& c) { return (size_t)(c.rp ? 2 : c.stages) * (c.bw + c.bt) * 8 * 16; }
+static size_t cfg_lds(const TileCfg& c) {
+  return c.rp ? (size_t)2 * (c.bw + c.bt) * 8 * 16 : (size_t)c.stages * (c.bw + c.bt) * (c.kd / 8) * 16;
+}
 
 // Fallback estimate for shapes outside the table: saturated throughput of the configuration, or the
 // time of one workgroup when there are fewer workgroups than CUs.
@@ -591,12 +636,15 @@ static double plan_cost(const TileCfg& c, int n, int Nw, int T, int K) {
   return ceil(units / slots) * t_unit * (bpc < 2 ? 1.0 : 1.6) + t_part;
 }
 
+// force_bw != 0 (the LM head): the tile must be force_bw weight rows split over exactly
+// kLmWaves waves along W, the layout the top-2 epilogue's cross-wave merge is written for.
+static bool lm_ok(const TileCfg& c, int force_bw) { return !force_bw || (c.bw == force_bw && c.ww == kLmWaves); }
+
 GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   GemmPlan best{0, 1, 0};
   bool found = false;
   for (const TunedShape& ts : kTuned)
-    if (ts.nw == Nw && ts.t == T && ts.k == K && ts.nsplit <= max_split &&
-        (!force_bw || kCfgs[ts.cfg].bw == force_bw)) {
+    if (ts.nw == Nw && ts.t == T && ts.k == K && ts.nsplit <= max_split && lm_ok(kCfgs[ts.cfg], force_bw)) {
       best.cfg = ts.cfg;
       best.nsplit = ts.nsplit;
       found = true;
@@ -606,7 +654,7 @@ GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
     double best_t = 1e30;
     const int nk = (K + 63) / 64;
     for (int ci = 0; ci < kNumCfgs; ++ci) {
-      if (force_bw && kCfgs[ci].bw != force_bw) continue;
+      if (!lm_ok(kCfgs[ci], force_bw)) continue;
       for (int n = 1; n <= max_split; ++n) {
         if (n > 1 && nk / n < 8) break;
         const double t = plan_cost(kCfgs[ci], n, Nw, T, K);
@@ -623,7 +671,7 @@ GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   return best;
 }
 
-template <int BW, int BT, int STAGES, class Epi, int WW = 2, int WT = 2>
+template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi>
 static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
                     const Epi& epi, hipStream_t s) {
   const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
@@ -633,8 +681,8 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   // over the units that turn out to be active) so inactive token tiles cost no dispatch.
   int grid = 8 * ((units + 7) / 8);
   if (t_count && grid > 8 * kCUs) grid = 8 * kCUs;
-  const size_t lds = (size_t)STAGES * (BW + BT) * 8 * 16;
-  auto kern = gemm_kernel<BW, BT, STAGES, WW, WT, Epi>;
+  const size_t lds = (size_t)STAGES * (BW + BT) * (KD / 8) * 16;
+  auto kern = gemm_kernel<BW, BT, KD, STAGES, WW, WT, Epi>;
   static bool attr_set = false;  // one flag per instantiation
   if (!attr_set) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -647,20 +695,24 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
 template <class Epi>
 static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
                      const Epi& epi, hipStream_t s) {
+  const int n = p.nsplit;
   switch (p.cfg) {
-    case 0: run_cfg<128, 128, 2, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 1: run_cfg<96, 192, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 2: run_cfg<192, 192, 3, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 3: run_cfg<64, 64, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 4: run_cfg<64, 64, 2, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 5: run_cfg<128, 64, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 6: run_cfg<128, 256, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 7: run_cfg<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 8: run_cfg<128, 128, 4, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 9: run_rp<96, 192, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 10: run_rp<192, 192, 2, Epi, 4, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    case 11: run_rp<128, 128, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
-    default: run_rp<64, 128, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, p.nsplit, epi, s); break;
+    case 0: run_cfg<128, 128, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 1: run_cfg<192, 192, 64, 3, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 2: run_cfg<64, 64, 64, 4, 2, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 3: run_cfg<128, 256, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 4: run_rp<96, 192, 3, Epi, 2, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 5: run_rp<192, 192, 2, Epi, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 6: run_rp<128, 128, 3, Epi, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 7: run_cfg<96, 192, 128, 2, 3, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 8: run_cfg<128, 96, 128, 2, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 9: run_cfg<160, 128, 128, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 10: run_cfg<96, 192, 128, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 11: run_cfg<192, 192, 64, 3, 4, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 12: run_cfg<128, 128, 128, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 13: run_cfg<64, 192, 128, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 14: run_cfg<128, 192, 128, 2, 4, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    default: run_cfg<128, 128, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
   }
 }
 
@@ -683,8 +735,8 @@ void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, floa
   run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, EpiF32{out}, s);
 }
 void gemm_lmhead(const bf16_t* W, const bf16_t* X, int V, int T, int K, const LmOut& o, hipStream_t s) {
-  static_assert(kLmTile == 128, "the LM-head vocabulary tile is the GEMM's weight tile");
-  run_plan(plan_gemm(V, T, K, kLmTile, 1), W, X, V, T, K, o.count, EpiLm<128, 2>{o}, s);
+  static_assert(kLmTile == 128 && kLmWaves == 2, "the LM-head vocabulary tile is the GEMM's weight tile");
+  run_plan(plan_gemm(V, T, K, kLmTile, 1), W, X, V, T, K, o.count, EpiLm<kLmTile, kLmWaves>{o}, s);
 }
 
 }  // namespace dcl
