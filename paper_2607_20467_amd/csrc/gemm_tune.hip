@@ -1,0 +1,105 @@
+// GEMM plan sweep (not part of the library): times every tile configuration / K-split with the
+// fused epilogue of each GEMM shape of the LLaDA-8B and Dream-7B workloads and prints the fastest
+// as lines of gemm_tuned.inc. Weights rotate through 3 GiB so no run is served from the MALL.
+//   hipcc --offload-arch=gfx950 -O3 -std=c++17 -I include -Xclang -target-feature \
+//         -Xclang -packed-fp32-ops paper_2607_20467_amd/csrc/gemm_tune.hip -o gemm_tune
+//   ./gemm_tune [shape index]
+#include "k_gemm.hip"
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+#include <string>
+using namespace dcl;
+#define CK(x) do { hipError_t e = (x); if (e != hipSuccess) { printf("HIP error %s at %d\n", hipGetErrorString(e), __LINE__); exit(1);} } while (0)
+__global__ void fill(bf16_t* p, size_t n, uint32_t seed) {
+  size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (i < n) { uint32_t h = (uint32_t)i * 2654435761u ^ seed; h ^= h >> 13; h *= 0x5bd1e995; p[i] = (h & 0x8000) | (0x3b80 + ((h >> 8) & 3) * 0x80) | (h & 0x7f); }
+}
+struct Shape { std::string name; int N, T, K; char kind; int H, Hkv, R; };
+int main(int argc, char** argv) {
+  const int only = argc > 1 ? atoi(argv[1]) : -1;
+  std::vector<Shape> shapes = {
+    {"LLaDA-8B 384 tok qkv", 12288, 384, 4096, 'q', 32, 32, 0}, {"LLaDA-8B 384 tok o", 4096, 384, 4096, 'r', 0, 0, 0},
+    {"LLaDA-8B 384 tok gu", 24576, 384, 4096, 's', 0, 0, 0}, {"LLaDA-8B 384 tok down", 4096, 384, 12288, 'r', 0, 0, 0},
+    {"LLaDA-8B 384 tok lm", 126464, 384, 4096, 'l', 0, 0, 256},
+    {"LLaDA-8B 8x64 tok qkv", 12288, 512, 4096, 'q', 32, 32, 0}, {"LLaDA-8B 8x64 tok o", 4096, 512, 4096, 'r', 0, 0, 0},
+    {"LLaDA-8B 8x64 tok gu", 24576, 512, 4096, 's', 0, 0, 0}, {"LLaDA-8B 8x64 tok down", 4096, 512, 12288, 'r', 0, 0, 0},
+    {"LLaDA-8B 8x64 tok lm", 126464, 512, 4096, 'l', 0, 0, 256},
+    {"LLaDA-8B 1280 tok qkv", 12288, 1280, 4096, 'q', 32, 32, 0}, {"LLaDA-8B 1280 tok o", 4096, 1280, 4096, 'r', 0, 0, 0},
+    {"LLaDA-8B 1280 tok gu", 24576, 1280, 4096, 's', 0, 0, 0}, {"LLaDA-8B 1280 tok down", 4096, 1280, 12288, 'r', 0, 0, 0},
+    {"LLaDA-8B 1280 tok lm", 126464, 1280, 4096, 'l', 0, 0, 960},
+    {"Dream-7B 4x768 tok qkv", 4608, 3072, 3584, 'q', 28, 4, 0}, {"Dream-7B 4x768 tok o", 3584, 3072, 3584, 'r', 0, 0, 0},
+    {"Dream-7B 4x768 tok gu", 37888, 3072, 3584, 's', 0, 0, 0}, {"Dream-7B 4x768 tok down", 3584, 3072, 18944, 'r', 0, 0, 0},
+    {"Dream-7B 4x768 tok lm", 152064, 3072, 3584, 'l', 0, 0, 2048},
+  };
+  size_t maxw = 0, maxx = 0, maxo = 0;
+  for (auto& s : shapes) { maxw = std::max(maxw, (size_t)s.N * s.K); maxx = std::max(maxx, (size_t)s.T * s.K); maxo = std::max(maxo, (size_t)s.N * s.T); }
+  bf16_t *W, *X, *q, *k, *vt, *a; float *r, *P, *pm1, *pm2, *ps; int32_t *pi1, *pi2, *cnt; float2* rope;
+  const size_t pool = std::max(maxw, (size_t)1536 << 20);  // elements: 3 GiB of weights, far beyond the 256 MB MALL
+  CK(hipMalloc(&W, pool * 2)); CK(hipMalloc(&X, maxx * 2));
+  CK(hipMalloc(&q, maxo * 2)); CK(hipMalloc(&k, maxo * 2)); CK(hipMalloc(&vt, maxo * 2 + (1 << 20))); CK(hipMalloc(&a, maxo * 2));
+  CK(hipMalloc(&r, maxo * 4)); CK(hipMalloc(&P, maxo * 4 * 4));
+  const size_t lmp = (size_t)3072 * (152064 / 128 + 1);
+  CK(hipMalloc(&pm1, lmp * 4)); CK(hipMalloc(&pm2, lmp * 4)); CK(hipMalloc(&ps, lmp * 4));
+  CK(hipMalloc(&pi1, lmp * 4)); CK(hipMalloc(&pi2, lmp * 4)); CK(hipMalloc(&cnt, 4));
+  CK(hipMalloc(&rope, (size_t)4096 * 64 * 8)); CK(hipMemset(rope, 0, (size_t)4096 * 64 * 8));
+  hipLaunchKernelGGL(fill, dim3((pool + 255) / 256), dim3(256), 0, 0, W, pool, 1u);
+  hipLaunchKernelGGL(fill, dim3((maxx + 255) / 256), dim3(256), 0, 0, X, maxx, 2u);
+  CK(hipDeviceSynchronize());
+  hipEvent_t e0, e1; CK(hipEventCreate(&e0)); CK(hipEventCreate(&e1));
+  for (size_t si = 0; si < shapes.size(); ++si) {
+    if (only >= 0 && (int)si != only) continue;
+    const Shape& s = shapes[si];
+    const int B = 1, S = s.T;
+    double best = 1e30; int bc = -1, bn = 1;
+    printf("%s: N %d T %d K %d (current plan cfg %d split %d)\n", s.name.c_str(), s.N, s.T, s.K,
+           plan_gemm(s.N, s.T, s.K, s.kind == 'l' ? kLmTile : 0, s.kind == 'r' ? kMaxSplit : 1).cfg,
+           plan_gemm(s.N, s.T, s.K, s.kind == 'l' ? kLmTile : 0, s.kind == 'r' ? kMaxSplit : 1).nsplit);
+    if (s.kind == 'l') { int R = s.R; CK(hipMemcpy(cnt, &R, 4, hipMemcpyHostToDevice)); }
+    for (int ci = 0; ci < kNumCfgs; ++ci) {
+      const TileCfg& c = kCfgs[ci];
+      if (s.kind == 'l' && (c.bw != 128 || c.ww != 2)) continue;
+      const int maxn = s.kind == 'r' ? 4 : 1;
+      for (int n = 1; n <= maxn; ++n) {
+        if (n > 1 && (s.K / 64) / n < 8) continue;
+        if (n > 1 && c.rp) continue;
+        GemmPlan p{ci, n, 0};
+        const size_t wsz = (size_t)s.N * s.K;
+        const int ncopy = (int)std::max<size_t>(1, pool / wsz);
+        int rot = 0;
+        auto run = [&]() {
+          const bf16_t* Wr = W + (size_t)(rot++ % ncopy) * wsz;
+          if (s.kind == 'q') {
+            QkvOut o{q, k, vt, nullptr, rope, s.H, s.Hkv, 128, S, (S + 7) / 8 * 8, 0};
+            run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiQkv{o}, 0);
+          } else if (s.kind == 's') {
+            run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiSwiglu{a}, 0);
+          } else if (s.kind == 'r') {
+            if (n > 1) run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiPartial{P, (size_t)s.T * s.N}, 0);
+            else run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiResid{r}, 0);
+          } else {
+            LmOut o{pm1, pm2, ps, pi1, pi2, (s.N + kLmTile - 1) / kLmTile, cnt};
+            run_plan(p, W, X, s.N, s.T, s.K, cnt, EpiLm<128, 2>{o}, 0);
+          }
+        };
+        for (int w = 0; w < 3; ++w) run();
+        CK(hipDeviceSynchronize());
+        const int reps = 20;
+        CK(hipEventRecord(e0, 0));
+        for (int rr = 0; rr < reps; ++rr) run();
+        CK(hipEventRecord(e1, 0)); CK(hipEventSynchronize(e1));
+        float ms; CK(hipEventElapsedTime(&ms, e0, e1));
+        const double us = 1000.0 * ms / reps;
+        // split-K slices are added by the next RMSNorm: charge their extra traffic (~2 x 4 B per slice)
+        const double pen = n > 1 ? (double)(n - 1) * s.T * s.N * 8 / 5.0e12 * 1e6 : 0.0;
+        printf("  cfg %2d (%3dx%3d k%3d s%d w%dx%d%s) split %d: %8.1f us (+%.1f slices)  %7.1f TFLOP/s\n", ci, c.bw, c.bt,
+               c.kd, c.stages, c.ww, c.wt, c.rp ? " rp" : "", n, us, pen,
+               2.0 * s.N * (s.kind == 'l' ? s.R : s.T) * s.K / us / 1e6);
+        if (us + pen < best) { best = us + pen; bc = ci; bn = n; }
+      }
+    }
+    printf("BEST {%d, %d, %d, %d, %d},  // %s: %.1f us\n", s.N, s.T, s.K, bc, bn, s.name.c_str(), best);
+    fflush(stdout);
+  }
+  return 0;
+}
