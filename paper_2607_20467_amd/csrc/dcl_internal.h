@@ -12,14 +12,29 @@ typedef uint16_t bf16_t;  // bfloat16 bit pattern
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-// float -> bfloat16, round to nearest even (finite inputs; NaN stays NaN).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7F800000u) == 0x7F800000u) return (bf16_t)((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// float -> bfloat16, round to nearest even, by gfx950's v_cvt_pk_bf16_f32. Checked on MI355X
+// against the bit-level definition (add 0x7fff + lsb, truncate) for all 2^32 inputs: identical
+// for every non-NaN value, denormals and infinities included; NaN stays NaN.
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+// Two conversions in one instruction: lo in bits 0-15, hi in bits 16-31.
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// One wave-wide global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4); lane i lands at
+// lds + 16 i, so `lds` must be wave-uniform. Issued from inline assembly with M0 = the LDS
+// destination: the compiler then neither counts the copy as outstanding LDS traffic (which makes
+// it wait for lgkmcnt(0) before every fragment read) nor inserts vmcnt(0) before LDS reads that
+// might alias it. Callers track completion themselves (s_waitcnt vmcnt + barrier).
+__device__ __forceinline__ void dma16(const void* g, const void* lds) {
+  const uint32_t m0v =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0v), "v"(g) : "memory", "m0");
+}
 
 // Packed-weight layout (byte offsets into the caller's weight buffer).
 struct LayerOffsets {

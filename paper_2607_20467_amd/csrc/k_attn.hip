@@ -23,6 +23,22 @@ __device__ __forceinline__ f32x4_t mfma16a(const bf16x8_t& a, const bf16x8_t& b,
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// op(v, v of lane ^ 16) and op(v, v of lane ^ 32) in every lane, through the gfx950 lane-swap
+// instructions (no LDS round trip). The swap of a register with itself leaves, per lane, the
+// value of both partners in the two results; op must be commutative.
+template <class Op>
+__device__ __forceinline__ float xor_lanes16(float v, Op op) {
+  const int b = __builtin_bit_cast(int, v);
+  const auto p = __builtin_amdgcn_permlane16_swap(b, b, false, false);
+  return op(__builtin_bit_cast(float, (int)p[0]), __builtin_bit_cast(float, (int)p[1]));
+}
+template <class Op>
+__device__ __forceinline__ float xor_lanes32(float v, Op op) {
+  const int b = __builtin_bit_cast(int, v);
+  const auto p = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return op(__builtin_bit_cast(float, (int)p[0]), __builtin_bit_cast(float, (int)p[1]));
+}
+
 template <int N>
 __device__ __forceinline__ void attn_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
@@ -95,7 +111,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
         if (j < P) src = vc + (size_t)d * P + j;
         else if (j < nkeys) src = vf + (size_t)d * a.Sp + (j - P);
       }
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(stage + q * 64), 16, 0, 0);
+      dma16(src, stage + q * 64);
     }
   };
 
@@ -130,30 +146,32 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
       }
     }
     float tmax = -INFINITY;
+    const bool tail = k0 + KT > nkeys;  // only the last tile holds keys past the end
 #pragma unroll
     for (int kt = 0; kt < KT / 16; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = k0 + 16 * kt + 4 * lg + r;
-        const float v = key < nkeys ? sc[kt][r] * a.scale_log2 : -INFINITY;
+        const float v = (!tail || key < nkeys) ? sc[kt][r] * a.scale_log2 : -INFINITY;
         sc[kt][r] = v;
         tmax = fmaxf(tmax, v);
       }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mn = fmaxf(m, tmax);
-    const float alpha = exp2f(m - mn);
+    // the four lane groups holding one query's keys: lanes l, l^16, l^32, l^48
+    tmax = xor_lanes16(tmax, [](float x, float y) { return fmaxf(x, y); });
+    tmax = xor_lanes32(tmax, [](float x, float y) { return fmaxf(x, y); });
+    const float mn = fmaxf(m, tmax);  // finite: every tile holds at least one key
+    const float alpha = __builtin_amdgcn_exp2f(m - mn);
     float psum = 0.f;
 #pragma unroll
     for (int kt = 0; kt < KT / 16; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float pv = exp2f(sc[kt][r] - mn);
+        const float pv = __builtin_amdgcn_exp2f(sc[kt][r] - mn);
         sc[kt][r] = pv;
         psum += pv;
       }
-    psum += __shfl_xor(psum, 16, 64);
-    psum += __shfl_xor(psum, 32, 64);
+    psum = xor_lanes16(psum, [](float x, float y) { return x + y; });
+    psum = xor_lanes32(psum, [](float x, float y) { return x + y; });
     l = l * alpha + psum;
     m = mn;
 #pragma unroll
@@ -166,9 +184,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
         const float p0 = sc[2 * s2 + (x >> 1)][(x & 1) * 2], p1 = sc[2 * s2 + (x >> 1)][(x & 1) * 2 + 1];
-        const bf16_t h0 = f2bf(p0), h1 = f2bf(p1);
-        hi[x] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        lo[x] = (uint32_t)f2bf(p0 - bf2f(h0)) | ((uint32_t)f2bf(p1 - bf2f(h1)) << 16);
+        hi[x] = f2bf2(p0, p1);
+        lo[x] = f2bf2(p0 - __uint_as_float(hi[x] << 16), p1 - __uint_as_float(hi[x] & 0xFFFF0000u));
       }
       const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
       const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
@@ -192,8 +209,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DH / 16; ++dt) {
       uint2 w;
-      w.x = (uint32_t)f2bf(o[dt][0] * inv) | ((uint32_t)f2bf(o[dt][1] * inv) << 16);
-      w.y = (uint32_t)f2bf(o[dt][2] * inv) | ((uint32_t)f2bf(o[dt][3] * inv) << 16);
+      w.x = f2bf2(o[dt][0] * inv, o[dt][1] * inv);
+      w.y = f2bf2(o[dt][2] * inv, o[dt][3] * inv);
       *reinterpret_cast<uint2*>(dst + 16 * dt) = w;
     }
   }

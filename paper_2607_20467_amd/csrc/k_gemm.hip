@@ -73,7 +73,7 @@ struct EpiSwiglu {
         const float g0 = acc[i][j][0], u0 = acc[i][j][1], g1 = acc[i][j][2], u1 = acc[i][j][3];
         const float h0 = g0 / (1.0f + __expf(-g0)) * u0;
         const float h1 = g1 / (1.0f + __expf(-g1)) * u1;
-        *reinterpret_cast<uint32_t*>(a + (size_t)t * F + (w >> 1)) = (uint32_t)f2bf(h0) | ((uint32_t)f2bf(h1) << 16);
+        *reinterpret_cast<uint32_t*>(a + (size_t)t * F + (w >> 1)) = f2bf2(h0, h1);
       }
     }
   }
@@ -113,8 +113,8 @@ struct EpiQkv {
           }
           bf16_t* base = isq ? o.q + (((size_t)b * o.H + head) * o.S + s) * dh
                              : o.k + (((size_t)b * o.Hkv + head) * o.S + s) * dh;
-          *reinterpret_cast<uint32_t*>(base + jp) = (uint32_t)f2bf(v0) | ((uint32_t)f2bf(v2) << 16);
-          *reinterpret_cast<uint32_t*>(base + half + jp) = (uint32_t)f2bf(v1) | ((uint32_t)f2bf(v3) << 16);
+          *reinterpret_cast<uint32_t*>(base + jp) = f2bf2(v0, v2);
+          *reinterpret_cast<uint32_t*>(base + half + jp) = f2bf2(v1, v3);
         } else {
           const int wl = w - qrows - krows;
           const int head = wl / dh, dd = wl - head * dh;
@@ -293,9 +293,9 @@ struct EpiLm {
 // buffered per 32-wide K substep: the LDS reads of substep s + 1 are in flight while the MFMAs of
 // substep s run, and the first substep of stage k + 1 is read across the stage boundary.
 //
-// The DMA instructions are issued from inline assembly (M0 = LDS destination of the wave), so
-// the compiler's wait-count pass does not treat them as pending LDS traffic and keeps its LDS
-// waits fine-grained; their completion is tracked here with vmcnt waits on this wave's own
+// The DMA instructions are issued through dma16 (inline assembly), so the compiler's wait-count
+// pass does not treat them as pending LDS traffic and keeps its LDS waits fine-grained; their
+// completion is tracked here with vmcnt waits on this wave's own
 // outstanding stages, and a bare s_barrier (no vmcnt(0) fence) publishes a stage to the other
 // waves. Vector-memory loads complete in issue order, and no other vector-memory load is issued
 // inside the K loop, so "at most n outstanding" means "all but the newest n landed".
@@ -313,13 +313,6 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-// One wave-wide 16-byte-per-lane copy global -> LDS; lane i lands at lds + 16 i.
-__device__ __forceinline__ void dma16(const void* g, const uint4* lds) {
-  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0v), "v"(g) : "memory", "m0");
-}
 
 template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi>
 __global__ void __launch_bounds__(WW * WT * 64)

@@ -50,12 +50,12 @@ __device__ __forceinline__ float wave_sum(float v) {
 // With nP > 0 the row first takes the K-split slices of the residual GEMM that produced it:
 // r + P[0] + ... + P[nP-1] (each [T, d], added in that order); without `rows` the sum is written
 // back to r (with `rows`, the final norm, r is not needed afterwards and stays as it is).
-template <int NV>
+template <int NV, int NP>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ r, const float* __restrict__ g,
                                                      bf16_t* __restrict__ u, int T, int d, float eps,
                                                      const int32_t* __restrict__ rows,
                                                      const int32_t* __restrict__ count,
-                                                     const float* __restrict__ P, int nP) {
+                                                     const float* __restrict__ P) {
   __shared__ float red[4];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int j = blockIdx.x;
@@ -80,18 +80,25 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ r, con
     const int c = tid + k * 256;
     v[k] = c < d4 ? x[c] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  if (nP > 0) {
-    for (int sp = 0; sp < nP; ++sp) {
+  if (NP > 0) {
+    // every slice load is issued before the first add (one memory round trip, not NP); the adds
+    // then run in split order, so the sum is the same bit pattern as a sequential fold
+    float4 q[NP > 0 ? NP : 1][NV];
+#pragma unroll
+    for (int sp = 0; sp < NP; ++sp) {
       const float4* ps = reinterpret_cast<const float4*>(P + ((size_t)sp * T + src) * d);
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
         const int c = tid + k * 256;
-        if (c < d4) {
-          const float4 q = ps[c];
-          v[k].x += q.x; v[k].y += q.y; v[k].z += q.z; v[k].w += q.w;
-        }
+        q[sp][k] = c < d4 ? ps[c] : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
+#pragma unroll
+    for (int sp = 0; sp < NP; ++sp)
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        v[k].x += q[sp][k].x; v[k].y += q[sp][k].y; v[k].z += q[sp][k].z; v[k].w += q[sp][k].w;
+      }
     if (!rows) {
 #pragma unroll
       for (int k = 0; k < NV; ++k) {
@@ -114,25 +121,34 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ r, con
     if (c < d4) {
       const float4 w = g4[c];
       uint2 o;
-      o.x = (uint32_t)f2bf(v[k].x * inv * w.x) | ((uint32_t)f2bf(v[k].y * inv * w.y) << 16);
-      o.y = (uint32_t)f2bf(v[k].z * inv * w.z) | ((uint32_t)f2bf(v[k].w * inv * w.w) << 16);
+      o.x = f2bf2(v[k].x * inv * w.x, v[k].y * inv * w.y);
+      o.y = f2bf2(v[k].z * inv * w.z, v[k].w * inv * w.w);
       *reinterpret_cast<uint2*>(y + 4 * c) = o;
     }
+  }
+}
+
+template <int NV>
+static void launch_rmsnorm_nv(float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
+                              const int32_t* count, const float* P, int nP, hipStream_t s) {
+  switch (nP) {
+    case 0: hipLaunchKernelGGL((rmsnorm_kernel<NV, 0>), dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P); break;
+    case 1: hipLaunchKernelGGL((rmsnorm_kernel<NV, 1>), dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P); break;
+    case 2: hipLaunchKernelGGL((rmsnorm_kernel<NV, 2>), dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P); break;
+    case 3: hipLaunchKernelGGL((rmsnorm_kernel<NV, 3>), dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P); break;
+    default: hipLaunchKernelGGL((rmsnorm_kernel<NV, 4>), dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P); break;
   }
 }
 
 void launch_rmsnorm(float* r, const float* g, bf16_t* u, int T, int d, float eps, const int32_t* rows,
                     const int32_t* count, const float* P, int nP, hipStream_t s) {
   if (T == 0) return;
+  static_assert(kMaxSplit <= 4, "rmsnorm folds at most four split-K slices");
   const int nv = (d / 4 + 255) / 256;
-  if (nv <= 1)
-    hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
-  else if (nv <= 2)
-    hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
-  else if (nv <= 4)
-    hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(T), dim3(256), 0, s, r, g, u, T, d, eps, rows, count, P, nP);
+  if (nv <= 1) launch_rmsnorm_nv<1>(r, g, u, T, d, eps, rows, count, P, nP, s);
+  else if (nv <= 2) launch_rmsnorm_nv<2>(r, g, u, T, d, eps, rows, count, P, nP, s);
+  else if (nv <= 4) launch_rmsnorm_nv<4>(r, g, u, T, d, eps, rows, count, P, nP, s);
+  else launch_rmsnorm_nv<8>(r, g, u, T, d, eps, rows, count, P, nP, s);
 }
 
 // ---------------------------------------------------------------- scored-row compaction
