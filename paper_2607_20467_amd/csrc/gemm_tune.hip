@@ -58,7 +58,7 @@ int main(int argc, char** argv) {
     if (s.kind == 'l') { int R = s.R; CK(hipMemcpy(cnt, &R, 4, hipMemcpyHostToDevice)); }
     for (int ci = 0; ci < kNumCfgs; ++ci) {
       const TileCfg& c = kCfgs[ci];
-      if (s.kind == 'l' && (c.bw != 128 || c.ww != 2)) continue;
+      if (s.kind == 'l' && !lm_ok(c, kLmTile)) continue;
       const int maxn = s.kind == 'r' ? 4 : 1;
       for (int n = 1; n <= maxn; ++n) {
         if (n > 1 && (s.K / 64) / n < 8) continue;

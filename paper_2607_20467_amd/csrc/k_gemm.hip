@@ -187,6 +187,7 @@ struct Part {
   float m1, m2, s;
   int i1, i2;
 };
+constexpr size_t kLmEpiLds = sizeof(Part) * kLmWaves * 256;  // static LDS of the LM-head epilogue
 __device__ __forceinline__ void top2_push(Part& p, float v, int id) {
   if (better(v, id, p.m1, p.i1)) {
     p.m2 = p.m1; p.i2 = p.i1; p.m1 = v; p.i1 = id;
@@ -597,10 +598,12 @@ static const TileCfg kCfgs[] = {
     {128, 128, 64, 3, 2, 4, 1},  {96, 192, 128, 2, 3, 4, 0},  {128, 96, 128, 2, 4, 2, 0},
     {160, 128, 128, 2, 2, 4, 0}, {96, 192, 128, 2, 2, 4, 0},  {192, 192, 64, 3, 4, 4, 0},
     {128, 128, 128, 2, 2, 4, 0}, {64, 192, 128, 2, 2, 4, 0},  {128, 192, 128, 2, 4, 4, 0},
-    {128, 128, 64, 3, 2, 4, 0},
+    {128, 128, 64, 3, 2, 4, 0},  {128, 256, 64, 3, 2, 8, 0},  {128, 192, 64, 3, 2, 4, 0},
+    {128, 256, 64, 2, 2, 8, 0},
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kCUs = 256;
+constexpr size_t kLdsBytes = 160 * 1024;  // LDS per CU (gfx950)
 
 // Measured choices for the GEMM shapes of the LLaDA-8B / Dream-7B workloads (weight rows, tokens, K).
 struct TunedShape {
@@ -631,7 +634,9 @@ static double plan_cost(const TileCfg& c, int n, int Nw, int T, int K) {
 
 // force_bw != 0 (the LM head): the tile must be force_bw weight rows split over exactly
 // kLmWaves waves along W, the layout the top-2 epilogue's cross-wave merge is written for.
-static bool lm_ok(const TileCfg& c, int force_bw) { return !force_bw || (c.bw == force_bw && c.ww == kLmWaves); }
+static bool lm_ok(const TileCfg& c, int force_bw) {
+  return !force_bw || (c.bw == force_bw && c.ww == kLmWaves && cfg_lds(c) + kLmEpiLds <= kLdsBytes);
+}
 
 GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   GemmPlan best{0, 1, 0};
@@ -676,11 +681,18 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   if (t_count && grid > 8 * kCUs) grid = 8 * kCUs;
   const size_t lds = (size_t)STAGES * (BW + BT) * (KD / 8) * 16;
   auto kern = gemm_kernel<BW, BT, KD, STAGES, WW, WT, Epi>;
-  static bool attr_set = false;  // one flag per instantiation
-  if (!attr_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)lds);
-    attr_set = true;
+  static int fits = -1;  // per instantiation: the ring plus the epilogue's static LDS fit in a CU
+  if (fits < 0) {
+    hipFuncAttributes at{};
+    fits = hipFuncGetAttributes(&at, reinterpret_cast<const void*>(kern)) == hipSuccess &&
+           at.sharedSizeBytes + lds <= kLdsBytes;
+    if (fits)
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds);
+  }
+  if (!fits) {  // never planned (plans respect kLdsBytes); keep a launch the runtime would reject off the GPU
+    run_cfg<128, 128, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, nsplit, epi, s);
+    return;
   }
   hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, epi);
 }
@@ -705,7 +717,10 @@ static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw
     case 12: run_cfg<128, 128, 128, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 13: run_cfg<64, 192, 128, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 14: run_cfg<128, 192, 128, 2, 4, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
-    default: run_cfg<128, 128, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 15: run_cfg<128, 128, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 16: run_cfg<128, 256, 64, 3, 2, 8>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 17: run_cfg<128, 192, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    default: run_cfg<128, 256, 64, 2, 2, 8>(W, X, Nw, T, K, t_count, n, epi, s); break;
   }
 }
 
