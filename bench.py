@@ -131,6 +131,18 @@ def pmc_summary(csv_path, copy_mib):
     return out
 
 
+def gpu_clock_mhz():
+    """Current shader clock reported by rocm-smi right after the timed steps (None if unavailable)."""
+    import re
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20).stdout
+    except Exception:
+        return None
+    m = re.search(r"sclk clock level:\s*\d+:\s*\((\d+)\s*Mhz\)", out, re.IGNORECASE)
+    return int(m.group(1)) if m else None
+
+
 def step_flops(w, R):
     per = step_work(w, R)
     L = w.geom.n_layers
@@ -234,11 +246,17 @@ def main():
         one_step()
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
+    # per-step HIP events on the launch stream (the whole-run clock below gives `value`)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         one_step()
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    step_ms = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    clock = gpu_clock_mhz()
     ms = 1000.0 * elapsed / args.steps
     steps_per_s = 1000.0 / ms
     flops = step_flops(w, R)
@@ -305,6 +323,9 @@ def main():
         "config": {"workload": f"{w.key}: {w.description}", "geometry": g.name, "batch": B, "seq_len": S,
                    "kv_prefix": w.kv_prefix, "scored_rows": R, "window": w.window, "tau_commit": w.tau_commit,
                    "tau_draft": w.tau_draft, "parallelism": "single GPU"},
+        "step_ms": {"median": round(float(np.median(step_ms)), 4), "p10": round(float(np.percentile(step_ms, 10)), 4),
+                    "p90": round(float(np.percentile(step_ms, 90)), 4)},
+        "gpu_sclk_mhz": clock,
         "scored_tokens_per_s": round(R * steps_per_s, 1),
         "mfma_util_pct": round(mfma_util, 2),
         "tflop_per_step": round(flops / 1e12, 4),

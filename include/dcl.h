@@ -154,6 +154,28 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
                                  dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,
                                  hipStream_t stream);
 
+/* Algorithm 1 (Section 3, Appendix A) end to end on the device: Eq. remasking of the first window,
+ * then repeated iterations of dcl_denoise_step (flags `score_flags`) followed by
+ * dcl_select_contiguous (tau_commit, tau_draft, `select_flags`, mask_id of the model), until every
+ * sequence has p >= gen_end or max_steps iterations ran. tokens [B, S] and p [B] (device) hold the
+ * state in and out; stats, K_raw, K_eff and ws are as for the two calls above (K_raw, K_eff may be
+ * NULL). k_hist (device int32 [L + 1], may be NULL) is incremented at K_eff once per sequence and
+ * iteration in which the sequence was unfinished; the caller clears it.
+ * p is copied to the host every `check_every` iterations (and after the last) to test for
+ * completion; iterations that run after every sequence finished change nothing. *steps_out (host)
+ * receives the number of iterations run. The first iteration is launched directly; the others
+ * replay one iteration captured into a HIP graph on a stream the call creates (the caller's stream
+ * may be the legacy null stream); with kernel-class profiling on, all run directly. The call
+ * returns after the device finished; the caller's stream is ordered after the work. It allocates
+ * only that stream, one event and the graph, and releases them before returning.
+ * 1 <= max_steps, 1 <= check_every; other argument rules as for the two calls. */
+dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S, int32_t* p,
+                        int32_t gen_end, const dcl_kv* kv, uint32_t score_flags, int32_t L,
+                        float tau_commit, float tau_draft, uint32_t select_flags, int32_t max_steps,
+                        int32_t check_every, dcl_row_stats stats, int32_t* K_raw, int32_t* K_eff,
+                        int32_t* k_hist, void* ws, size_t ws_bytes, int32_t* steps_out,
+                        hipStream_t stream);
+
 /* Workspace bytes for dcl_score_hidden over n rows; 0 if the arguments are invalid. */
 size_t dcl_score_workspace_bytes(dcl_model_t model, int32_t n);
 

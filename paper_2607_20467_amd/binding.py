@@ -77,6 +77,8 @@ def load_library():
                                             vp, sz, vp]),
         "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, f32, f32, i32, DclRowStats, vp, vp,
                                                  u32, vp]),
+        "dcl_generate": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, i32, f32, f32, u32,
+                                        i32, i32, DclRowStats, vp, vp, vp, vp, sz, ctypes.POINTER(i32), vp]),
         "dcl_score_workspace_bytes": (sz, [vp, i32]),
         "dcl_profile_enable": (ctypes.c_int, [i32]),
         "dcl_profile_read": (ctypes.c_int, [ctypes.POINTER(DclProfile)]),
@@ -174,6 +176,20 @@ def dcl_select_contiguous(tokens, B: int, S: int, p, gen_end: int, L: int, tau_c
     _check(load_library().dcl_select_contiguous(_ptr(tokens), B, S, _ptr(p), gen_end, L, tau_commit, tau_draft,
                                                 mask_id, _stats(stats), _ptr(k_raw), _ptr(k_eff), flags,
                                                 _stream(stream)), "dcl_select_contiguous")
+
+
+def dcl_generate(model: int, tokens, B: int, S: int, p, gen_end: int, kv, score_flags: int, L: int,
+                 tau_commit: float, tau_draft: float, select_flags: int, max_steps: int, check_every: int, stats,
+                 k_raw, k_eff, k_hist, ws, ws_bytes: int, stream=None) -> int:
+    """Returns the number of iterations run."""
+    kvp, keep = _kv(kv)
+    steps = ctypes.c_int32(0)
+    _check(load_library().dcl_generate(model, _ptr(tokens), B, S, _ptr(p), gen_end, kvp, score_flags, L, tau_commit,
+                                       tau_draft, select_flags, max_steps, check_every, _stats(stats), _ptr(k_raw),
+                                       _ptr(k_eff), _ptr(k_hist), _ptr(ws), ws_bytes, ctypes.byref(steps),
+                                       _stream(stream)), "dcl_generate")
+    del keep
+    return steps.value
 
 
 def dcl_profile_enable(on: bool) -> None:

@@ -283,6 +283,69 @@ int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_k
   return pending;
 }
 
+dcl_status check_denoise_args(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const int32_t* p,
+                              int32_t gen_end, const dcl_kv* kv, uint32_t flags, const dcl_row_stats& out, void* ws,
+                              size_t ws_bytes) {
+  dcl_status st = check_step_args(m, tokens, B, S, kv, ws, ws_bytes);
+  if (st != DCL_OK) return st;
+  if (!p) return fail(DCL_E_ARG, "p is NULL");
+  if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
+  if (flags & ~(uint32_t)DCL_SCORE_ALL_UNCOMMITTED) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  if (!out.top1 || !out.top2 || !out.conf || !out.p2 || !out.lse) return fail(DCL_E_ARG, "an output array is NULL");
+  return DCL_OK;
+}
+
+// a2-a10 on `stream` (arguments already checked).
+void enqueue_denoise(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const int32_t* p, int32_t gen_end,
+                     const dcl_kv* kv, uint32_t flags, const dcl_row_stats& out, void* ws, hipStream_t stream) {
+  const dcl_config& c = m->cfg;
+  const StepLayout L = step_layout(c, B, S);
+  const int pending = run_forward(m, tokens, B, S, kv, ws, L, stream);
+  int32_t* rows = at<int32_t>(ws, L.rows);
+  int32_t* count = at<int32_t>(ws, L.count);
+  hipStream_t s = stream;
+  {
+    PROF(P_COMPACT);
+    launch_compact(tokens, p, B, S, gen_end, c.mask_id, (flags & DCL_SCORE_ALL_UNCOMMITTED) ? 1 : 0, rows, count, out,
+                   stream);
+  }
+  bf16_t* hf = at<bf16_t>(ws, L.hf);
+  {
+    PROF(P_NORM);
+    launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count,
+                   at<float>(ws, L.part), pending, stream);
+  }
+  LmOut lo;
+  lo.pm1 = at<float>(ws, L.pm1);
+  lo.pi1 = at<int32_t>(ws, L.pi1);
+  lo.pm2 = at<float>(ws, L.pm2);
+  lo.pi2 = at<int32_t>(ws, L.pi2);
+  lo.ps = at<float>(ws, L.ps);
+  lo.n_vt = L.n_vt;
+  lo.count = count;
+  {
+    PROF(P_LM);
+    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
+  }
+  {
+    PROF(P_MERGE);
+    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, L.T, out, stream);
+  }
+}
+
+dcl_status check_select_args(const int32_t* tokens, int32_t B, int32_t S, const int32_t* p, int32_t gen_end,
+                             int32_t L, float tau_commit, float tau_draft, const dcl_row_stats& in, uint32_t flags) {
+  if (!tokens || !p) return fail(DCL_E_ARG, "tokens / p is NULL");
+  if (!in.top1 || !in.conf) return fail(DCL_E_ARG, "in.top1 / in.conf is NULL");
+  if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
+  if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
+  if (L < 1) return fail(DCL_E_ARG, "window L=%d must be >= 1", L);
+  if (!(tau_commit >= 0.f && tau_commit <= 1.f)) return fail(DCL_E_ARG, "tau_commit %g outside [0, 1]", tau_commit);
+  if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
+  if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL)) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  return DCL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -415,64 +478,22 @@ size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_p
   return step_layout(m->cfg, B, S).total;
 }
 
+
 dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S, const int32_t* p,
                             int32_t gen_end, const dcl_kv* kv, uint32_t flags, dcl_row_stats out, void* ws,
                             size_t ws_bytes, hipStream_t stream) {
   Model* m = reinterpret_cast<Model*>(model);
-  dcl_status st = check_step_args(m, tokens, B, S, kv, ws, ws_bytes);
+  dcl_status st = check_denoise_args(m, tokens, B, S, p, gen_end, kv, flags, out, ws, ws_bytes);
   if (st != DCL_OK) return st;
-  if (!p) return fail(DCL_E_ARG, "p is NULL");
-  if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
-  if (flags & ~(uint32_t)DCL_SCORE_ALL_UNCOMMITTED) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
-  if (!out.top1 || !out.top2 || !out.conf || !out.p2 || !out.lse) return fail(DCL_E_ARG, "an output array is NULL");
-  const dcl_config& c = m->cfg;
-  const StepLayout L = step_layout(c, B, S);
   (void)hipGetLastError();  // clear a stale error so the check below reports this call's launches
-  const int pending = run_forward(m, tokens, B, S, kv, ws, L, stream);
-  int32_t* rows = at<int32_t>(ws, L.rows);
-  int32_t* count = at<int32_t>(ws, L.count);
-  hipStream_t s = stream;
-  {
-    PROF(P_COMPACT);
-    launch_compact(tokens, p, B, S, gen_end, c.mask_id, (flags & DCL_SCORE_ALL_UNCOMMITTED) ? 1 : 0, rows, count, out,
-                   stream);
-  }
-  bf16_t* hf = at<bf16_t>(ws, L.hf);
-  {
-    PROF(P_NORM);
-    launch_rmsnorm(at<float>(ws, L.r), at<float>(m->wbuf, m->lay.gf), hf, L.T, c.d_model, c.rms_eps, rows, count,
-                   at<float>(ws, L.part), pending, stream);
-  }
-  LmOut lo;
-  lo.pm1 = at<float>(ws, L.pm1);
-  lo.pi1 = at<int32_t>(ws, L.pi1);
-  lo.pm2 = at<float>(ws, L.pm2);
-  lo.pi2 = at<int32_t>(ws, L.pi2);
-  lo.ps = at<float>(ws, L.ps);
-  lo.n_vt = L.n_vt;
-  lo.count = count;
-  {
-    PROF(P_LM);
-    gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
-  }
-  {
-    PROF(P_MERGE);
-    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, L.T, out, stream);
-  }
+  enqueue_denoise(m, tokens, B, S, p, gen_end, kv, flags, out, ws, stream);
   return hip_check(hipGetLastError(), "denoise_step launch");
 }
-
 dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end, int32_t L,
                                  float tau_commit, float tau_draft, int32_t mask_id, dcl_row_stats in,
                                  int32_t* K_raw, int32_t* K_eff, uint32_t flags, hipStream_t stream) {
-  if (!tokens || !p) return fail(DCL_E_ARG, "tokens / p is NULL");
-  if (!in.top1 || !in.conf) return fail(DCL_E_ARG, "in.top1 / in.conf is NULL");
-  if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
-  if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
-  if (L < 1) return fail(DCL_E_ARG, "window L=%d must be >= 1", L);
-  if (!(tau_commit >= 0.f && tau_commit <= 1.f)) return fail(DCL_E_ARG, "tau_commit %g outside [0, 1]", tau_commit);
-  if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
-  if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL)) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  dcl_status st = check_select_args(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, in, flags);
+  if (st != DCL_OK) return st;
   (void)hipGetLastError();
   {
     hipStream_t s = stream;
@@ -480,6 +501,93 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
     launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, in, K_raw, K_eff, flags, stream);
   }
   return hip_check(hipGetLastError(), "select launch");
+}
+
+dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end,
+                        const dcl_kv* kv, uint32_t score_flags, int32_t L, float tau_commit, float tau_draft,
+                        uint32_t select_flags, int32_t max_steps, int32_t check_every, dcl_row_stats stats,
+                        int32_t* K_raw, int32_t* K_eff, int32_t* k_hist, void* ws, size_t ws_bytes,
+                        int32_t* steps_out, hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  dcl_status st = check_denoise_args(m, tokens, B, S, p, gen_end, kv, score_flags, stats, ws, ws_bytes);
+  if (st != DCL_OK) return st;
+  st = check_select_args(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, stats, select_flags);
+  if (st != DCL_OK) return st;
+  if (max_steps < 1 || check_every < 1) return fail(DCL_E_ARG, "max_steps %d and check_every %d must be >= 1",
+                                                    max_steps, check_every);
+  if (!steps_out) return fail(DCL_E_ARG, "steps_out is NULL");
+  *steps_out = 0;
+  const int mask_id = m->cfg.mask_id;
+  (void)hipGetLastError();
+
+  // A private stream (the caller's may be the legacy null stream, which cannot be captured),
+  // ordered after the caller's stream on entry and before it on return.
+  hipStream_t gs = nullptr;
+  hipEvent_t ev = nullptr;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  std::vector<int32_t> ph(B);
+  int n = 0;
+  bool done = false;
+  auto iteration = [&](hipStream_t q) {
+    enqueue_denoise(m, tokens, B, S, p, gen_end, kv, score_flags, stats, ws, q);
+    hipStream_t s = q;
+    PROF(P_SELECT);
+    launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, stats, K_raw, K_eff, select_flags, q,
+                  k_hist);
+  };
+  auto check = [&]() -> dcl_status {  // host copy of p: done when every sequence reached gen_end
+    dcl_status e = hip_check(hipMemcpyAsync(ph.data(), p, (size_t)B * sizeof(int32_t), hipMemcpyDeviceToHost, gs),
+                             "hipMemcpyAsync(p)");
+    if (e == DCL_OK) e = hip_check(hipStreamSynchronize(gs), "hipStreamSynchronize");
+    if (e != DCL_OK) return e;
+    done = true;
+    for (int b = 0; b < B; ++b) done = done && (ph[b] < 0 || ph[b] >= gen_end);
+    return DCL_OK;
+  };
+  st = hip_check(hipStreamCreateWithFlags(&gs, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+  if (st == DCL_OK) st = hip_check(hipEventCreateWithFlags(&ev, hipEventDisableTiming), "hipEventCreate");
+  if (st == DCL_OK) st = hip_check(hipEventRecord(ev, stream), "hipEventRecord");
+  if (st == DCL_OK) st = hip_check(hipStreamWaitEvent(gs, ev, 0), "hipStreamWaitEvent");
+  if (st == DCL_OK) {
+    // Algorithm 1's loop-top draft invalidation for the first iteration; later ones end with it
+    launch_remask(tokens, B, S, p, gen_end, L, mask_id, gs);
+    st = check();
+  }
+  // The first iteration runs eagerly (it also performs every one-time kernel set-up, which must not
+  // happen under capture); later ones replay one captured iteration. With kernel-class profiling on,
+  // every iteration runs eagerly so each launch keeps its event pair.
+  while (st == DCL_OK && !done && n < max_steps) {
+    if (n > 0 && !exec && !g_prof.on) {
+      st = hip_check(hipStreamBeginCapture(gs, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+      if (st != DCL_OK) break;
+      iteration(gs);
+      const hipError_t launch_err = hipGetLastError();
+      st = hip_check(hipStreamEndCapture(gs, &graph), "hipStreamEndCapture");
+      if (st == DCL_OK) st = hip_check(launch_err, "captured iteration launch");
+      if (st == DCL_OK) st = hip_check(hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0), "hipGraphInstantiate");
+      if (st != DCL_OK) break;
+    }
+    if (exec) st = hip_check(hipGraphLaunch(exec, gs), "hipGraphLaunch");
+    else {
+      iteration(gs);
+      st = hip_check(hipGetLastError(), "iteration launch");
+    }
+    if (st != DCL_OK) break;
+    ++n;
+    if (n % check_every == 0 || n == max_steps) st = check();
+  }
+  *steps_out = n;
+  if (gs) {
+    if (st == DCL_OK) st = hip_check(hipEventRecord(ev, gs), "hipEventRecord");
+    if (st == DCL_OK) st = hip_check(hipStreamWaitEvent(stream, ev, 0), "hipStreamWaitEvent");
+    (void)hipStreamSynchronize(gs);
+  }
+  if (exec) (void)hipGraphExecDestroy(exec);
+  if (graph) (void)hipGraphDestroy(graph);
+  if (ev) (void)hipEventDestroy(ev);
+  if (gs) (void)hipStreamDestroy(gs);
+  return st;
 }
 
 struct ScoreLayout {

@@ -78,7 +78,9 @@ void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const 
 void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s);
 void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c,
                    float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
-                   uint32_t flags, hipStream_t s);
+                   uint32_t flags, hipStream_t s, int32_t* k_hist = nullptr);
+void launch_remask(int32_t* tokens, int B, int S, const int32_t* p, int gen_end, int L, int mask_id,
+                   hipStream_t s);
 void launch_pack_rows(const void* src, int src_dtype, bf16_t* dst, int rows, int cols, int mode,
                       int dh, int dst_row0, hipStream_t s);
 void launch_pack_vec(const void* src, int src_dtype, float* dst, int n, int mode, int dh, int dst0,

@@ -73,12 +73,14 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ r, con
     return;
   }
   float4* x = reinterpret_cast<float4*>(r + (size_t)src * d);
-  float4 v[NV];
+  const float4* g4 = reinterpret_cast<const float4*>(g);
+  float4 v[NV], gv[NV];  // the gains are loaded with the row, not after the reduction
   float ss = 0.f;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const int c = tid + k * 256;
     v[k] = c < d4 ? x[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    gv[k] = c < d4 ? g4[c] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if (NP > 0) {
     // every slice load is issued before the first add (one memory round trip, not NP); the adds
@@ -114,12 +116,11 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ r, con
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  const float4* g4 = reinterpret_cast<const float4*>(g);
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const int c = tid + k * 256;
     if (c < d4) {
-      const float4 w = g4[c];
+      const float4 w = gv[k];
       uint2 o;
       o.x = f2bf2(v[k].x * inv * w.x, v[k].y * inv * w.y);
       o.y = f2bf2(v[k].z * inv * w.z, v[k].w * inv * w.w);
@@ -285,7 +286,8 @@ void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s) {
 __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ tokens, int S, int32_t* __restrict__ p,
                                                     int gen_end, int L, float tau_c, float tau_d, int mask_id,
                                                     dcl_row_stats st, int32_t* __restrict__ k_raw,
-                                                    int32_t* __restrict__ k_eff, uint32_t flags) {
+                                                    int32_t* __restrict__ k_eff, uint32_t flags,
+                                                    int32_t* __restrict__ k_hist) {
   __shared__ int red[4];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   int32_t* x = tokens + (size_t)b * S;
@@ -325,13 +327,30 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
     p[b] = pn;
     if (k_raw) k_raw[b] = K;
     if (k_eff) k_eff[b] = Ke;
+    if (k_hist) atomicAdd(&k_hist[Ke], 1);  // Ke <= L_eff <= L: histogram of [L + 1] bins
   }
 }
 
+// Step (i) alone (Eq. remasking): x[b, p_b : min(p_b + L, gen_end)) = mask_id for every sequence
+// with 0 <= p_b < gen_end; one workgroup per sequence.
+__global__ void __launch_bounds__(256) remask_kernel(int32_t* __restrict__ tokens, int S,
+                                                    const int32_t* __restrict__ p, int gen_end, int L,
+                                                    int mask_id) {
+  const int b = blockIdx.x;
+  const int pb = p[b];
+  if (pb < 0 || pb >= gen_end) return;
+  const int stop = (int)min((long)pb + L, (long)gen_end);
+  for (int j = pb + (int)threadIdx.x; j < stop; j += 256) tokens[(size_t)b * S + j] = mask_id;
+}
+
 void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c, float tau_d,
-                   int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff, uint32_t flags, hipStream_t s) {
+                   int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff, uint32_t flags, hipStream_t s,
+                   int32_t* k_hist) {
   hipLaunchKernelGGL(select_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, tau_c, tau_d, mask_id, st,
-                     k_raw, k_eff, flags);
+                     k_raw, k_eff, flags, k_hist);
+}
+void launch_remask(int32_t* tokens, int B, int S, const int32_t* p, int gen_end, int L, int mask_id, hipStream_t s) {
+  hipLaunchKernelGGL(remask_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, mask_id);
 }
 
 // ---------------------------------------------------------------- weight packing (load time)

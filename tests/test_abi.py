@@ -79,6 +79,10 @@ def test_step_and_select_argument_checks_without_gpu(dcl):
         # weights not loaded
         r = lib.dcl_denoise_step(m, 8, 1, 384, 8, 384, None, 0, st, 256, 1 << 40, None)
         assert r == 5 and "not loaded" in dcl.dcl_last_error()
+        steps = ctypes.c_int32(-1)
+        r = lib.dcl_generate(m, 8, 1, 384, 8, 384, None, 0, 32, 0.7, 0.98, 0, 10, 1, st, None, None, None, 256,
+                             1 << 40, ctypes.byref(steps), None)
+        assert r == 5 and "not loaded" in dcl.dcl_last_error()
         # load: misaligned / too small / wrong count
         arr = (ctypes.c_void_p * 3)(1, 2, 3)
         assert lib.dcl_load_weights(m, 3, 1 << 40, arr, 3, 1, None) == 1

@@ -1,0 +1,145 @@
+"""dcl_generate (Algorithm 1 on the device, iterations replayed from a captured HIP graph) against
+the eager loop of dcl_denoise_step + dcl_select_contiguous on the same state.
+
+The eager loop is itself checked against the float64 oracle at every iteration
+(test_gpu_step.py::test_full_loop_matches_oracle_every_iteration); here every replay of the graph
+must reproduce it bit for bit: tokens, p, K_raw, K_eff after every iteration count, with the
+program's own eager work and host synchronisations between the replays."""
+import numpy as np
+import pytest
+
+import synth
+
+from helpers import runner_for, to_dev
+
+pytestmark = pytest.mark.gpu
+
+W = synth.WORKLOADS
+_cache = {}
+
+
+def _setup(key, gen_len=48, batch=None):
+    if key not in _cache:
+        w = W[key]
+        stored = synth.make_weights(w.geom)
+        _cache[key] = (w, runner_for(w, stored))
+    w, run = _cache[key]
+    prompt = synth.prompts(w)
+    if batch is not None:
+        prompt = prompt[:batch]
+    N = prompt.shape[1]
+    x = np.concatenate([prompt, np.full((prompt.shape[0], gen_len), w.geom.mask_id)], 1).astype(np.int32)
+    p = np.full(prompt.shape[0], N, np.int32)
+    return w, run, x, p
+
+
+def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0):
+    """States after each of n_iter eager iterations (device-resident, synchronised between them)."""
+    import torch
+    import paper_2607_20467_amd as dcl
+    B, S = x0.shape
+    tok, p = to_dev(x0), to_dev(p0)
+    # Algorithm 1's loop-top remask of the first window (the initial masks already cover it)
+    xs = tok.cpu().numpy()
+    for b in range(B):
+        xs[b, p0[b]:min(p0[b] + L, S)] = w.geom.mask_id
+    tok.copy_(to_dev(xs))
+    st = run.new_stats(B, S)
+    kr = torch.zeros(B, dtype=torch.int32, device="cuda")
+    ke = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = []
+    for _ in range(n_iter):
+        run.step(tok, p, S, stats=st, flags=score_flags)
+        dcl.dcl_select_contiguous(tok, B, S, p, S, L, tc, td, w.geom.mask_id, st, kr, ke, select_flags)
+        torch.cuda.synchronize()
+        out.append((tok.cpu().numpy(), p.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()))
+    return out
+
+
+def _generate(run, w, x0, p0, L, tc, td, max_steps, check_every=1, score_flags=0, select_flags=0, hist=None):
+    import torch
+    import paper_2607_20467_amd as dcl
+    B, S = x0.shape
+    tok, p = to_dev(x0), to_dev(p0)
+    st = run.new_stats(B, S)
+    kr = torch.zeros(B, dtype=torch.int32, device="cuda")
+    ke = torch.zeros(B, dtype=torch.int32, device="cuda")
+    ws, n = run.workspace(B, S)
+    steps = dcl.dcl_generate(run.model, tok, B, S, p, S, None, score_flags, L, tc, td, select_flags, max_steps,
+                             check_every, st, kr, ke, hist, ws, n)
+    torch.cuda.synchronize()
+    return steps, tok.cpu().numpy(), p.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()
+
+
+def test_every_replay_matches_the_eager_loop():
+    w, run, x0, p0 = _setup("c1s")
+    L, tc, td = 16, 0.7, 0.9
+    S = x0.shape[1]
+    ref = _eager(run, w, x0, p0, L, tc, td, 48)
+    n_done = next(i + 1 for i, (_, p, _, _) in enumerate(ref) if (p >= S).all())
+    print("eager loop finished in", n_done, "iterations", flush=True)
+    for k in range(1, n_done + 1):
+        steps, tok, p, kr, ke = _generate(run, w, x0, p0, L, tc, td, max_steps=k)
+        assert steps == k
+        rt, rp, rkr, rke = ref[k - 1]
+        np.testing.assert_array_equal(tok, rt, err_msg=f"tokens after {k} iterations")
+        np.testing.assert_array_equal(p, rp, err_msg=f"p after {k} iterations")
+        np.testing.assert_array_equal(kr, rkr, err_msg=f"K_raw after {k} iterations")
+        np.testing.assert_array_equal(ke, rke, err_msg=f"K_eff after {k} iterations")
+    # run to completion: stops at the first iteration where every p reached gen_end
+    steps, tok, p, _, _ = _generate(run, w, x0, p0, L, tc, td, max_steps=1000)
+    assert steps == n_done and (p == S).all()
+    np.testing.assert_array_equal(tok, ref[n_done - 1][0])
+
+
+def test_check_every_and_histogram():
+    import torch
+    w, run, x0, p0 = _setup("c1s")
+    L, tc, td = 16, 0.6, 0.95
+    S = x0.shape[1]
+    ref = _eager(run, w, x0, p0, L, tc, td, 48)
+    n_done = next(i + 1 for i, (_, p, _, _) in enumerate(ref) if (p >= S).all())
+    hist = torch.zeros(L + 1, dtype=torch.int32, device="cuda")
+    steps, tok, p, _, _ = _generate(run, w, x0, p0, L, tc, td, max_steps=1000, check_every=5, hist=hist)
+    # completion is seen at the next multiple of 5; the extra iterations change nothing
+    assert steps == -(-n_done // 5) * 5
+    np.testing.assert_array_equal(tok, ref[n_done - 1][0])
+    np.testing.assert_array_equal(p, ref[n_done - 1][1])
+    # histogram: one count per (sequence, iteration) while the sequence was unfinished
+    want = np.zeros(L + 1, np.int64)
+    p_prev = p0
+    for _, pk, _, kek in ref[:n_done]:
+        for b in range(len(p_prev)):
+            if p_prev[b] < S:
+                want[kek[b]] += 1
+        p_prev = pk
+    np.testing.assert_array_equal(hist.cpu().numpy(), want)
+
+
+def test_profiled_generate_runs_eagerly_and_agrees():
+    import paper_2607_20467_amd as dcl
+    w, run, x0, p0 = _setup("c1s")
+    L, tc, td = 16, 0.7, 0.9
+    a = _generate(run, w, x0, p0, L, tc, td, max_steps=1000)
+    dcl.dcl_profile_enable(True)
+    try:
+        b = _generate(run, w, x0, p0, L, tc, td, max_steps=1000)
+        prof = dcl.dcl_profile_read()
+    finally:
+        dcl.dcl_profile_enable(False)
+    assert a[0] == b[0]
+    for u, v in zip(a[1:], b[1:]):
+        np.testing.assert_array_equal(u, v)
+    assert prof["select"][0] == b[0]  # one select launch per iteration, each with its event pair
+
+
+def test_score_all_mode_replays_match():
+    import paper_2607_20467_amd as dcl
+    w, run, x0, p0 = _setup("c1s")
+    L, tc, td = 16, 0.7, 0.9
+    sf, sel = dcl.DCL_SCORE_ALL_UNCOMMITTED, dcl.DCL_SEL_SCORE_ALL
+    ref = _eager(run, w, x0, p0, L, tc, td, 6, score_flags=sf, select_flags=sel)
+    steps, tok, p, kr, ke = _generate(run, w, x0, p0, L, tc, td, max_steps=6, score_flags=sf, select_flags=sel)
+    assert steps == 6
+    np.testing.assert_array_equal(tok, ref[-1][0])
+    np.testing.assert_array_equal(p, ref[-1][1])
