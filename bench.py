@@ -185,6 +185,7 @@ def main():
     ap.add_argument("--workload", default="c2", help="synth workload key (c2 = LLaDA-8B shape, B1, S384)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the event-timed kernel-class pass")
+    ap.add_argument("--no-generate", action="store_true", help="skip the end-to-end decode (dcl_generate) run")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB (hardware-counter calibration)")
     ap.add_argument("--pmc-summary", metavar="CSV", help="summarise a rocprofv3 --pmc counter_collection.csv "
@@ -299,6 +300,29 @@ def main():
                     "flop_per_launch": per[dom], "algorithmic_bytes_per_launch": alg_bytes[dom],
                     "avg_launch_us": classes[dom]["avg_us"]}
 
+    gen = None
+    if not args.no_generate:
+        # Algorithm 1 end to end from the workload's initial state (dcl_generate: graph-replayed
+        # iterations, completion checked on the host after each one)
+        torch.cuda.synchronize()
+        tok.copy_(tok0)
+        p.copy_(p0)
+        hist = torch.zeros(w.window + 1, dtype=torch.int32, device="cuda")
+        max_steps = int(w.gen_end - p_h.min())
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        n_it = dcl.dcl_generate(run.model, tok, B, S, p, w.gen_end, kv, 0, w.window, w.tau_commit, w.tau_draft, 0,
+                                max_steps, 1, stats, k_raw, k_eff, hist, ws, ws_bytes, stream)
+        torch.cuda.synchronize()
+        t_gen = time.perf_counter() - t1
+        new_tok = int((w.gen_end - p_h).clip(min=0).sum())
+        done = bool((p.cpu().numpy() >= w.gen_end).all())
+        gen = {"iterations": n_it, "finished": done, "tokens": new_tok, "seconds": round(t_gen, 4),
+               "tokens_per_s": round(new_tok / t_gen, 1), "tokens_per_iteration": round(new_tok / max(n_it, 1), 3),
+               "ms_per_iteration": round(1000 * t_gen / max(n_it, 1), 4), "k_eff_hist": hist.cpu().tolist()}
+        log(f"generation: {n_it} iterations for {new_tok} tokens in {t_gen:.3f} s "
+            f"({new_tok / t_gen:.0f} tok/s, {1000 * t_gen / max(n_it, 1):.2f} ms/iteration)")
+
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * 1024 * 1024 // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -331,6 +355,7 @@ def main():
         "tflop_per_step": round(flops / 1e12, 4),
         "roofline": roofline,
         "kernel_classes": classes,
+        "generation": gen,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
