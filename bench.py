@@ -186,6 +186,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the event-timed kernel-class pass")
     ap.add_argument("--no-generate", action="store_true", help="skip the end-to-end decode (dcl_generate) run")
+    ap.add_argument("--select", choices=("dcv", "noncontiguous", "chain-drafts"), default="dcv",
+                    help="selection rule: Dynamic Contiguous Verification with drafts (default), the independent "
+                         "threshold rule, or drafts restricted to the leading chain")
+    ap.add_argument("--score-all", action="store_true", help="score every uncommitted position, not only masks")
+    ap.add_argument("--suppress-mask", action="store_true", help="leave the [MASK] id out of the vocabulary")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB (hardware-counter calibration)")
     ap.add_argument("--pmc-summary", metavar="CSV", help="summarise a rocprofv3 --pmc counter_collection.csv "
@@ -218,7 +223,12 @@ def main():
     log(f"loaded weights into HBM in {time.perf_counter() - t:.1f} s")
     tok_h, p_h = synth.initial_state(w)
     B, S = tok_h.shape
-    R = int(((tok_h == g.mask_id) & (np.arange(S)[None] >= p_h[:, None]) & (np.arange(S)[None] < w.gen_end)).sum())
+    inside = (np.arange(S)[None] >= p_h[:, None]) & (np.arange(S)[None] < w.gen_end)
+    R = int((inside if args.score_all else inside & (tok_h == g.mask_id)).sum())
+    score_flags = (dcl.DCL_SCORE_ALL_UNCOMMITTED if args.score_all else 0) | \
+        (dcl.DCL_SCORE_SUPPRESS_MASK if args.suppress_mask else 0)
+    sel_flags = (dcl.DCL_SEL_SCORE_ALL if args.score_all else 0) | \
+        {"dcv": 0, "noncontiguous": dcl.DCL_SEL_NONCONTIGUOUS, "chain-drafts": dcl.DCL_SEL_CONTIGUOUS_DRAFTS}[args.select]
     tok0 = torch.from_numpy(tok_h).cuda()
     p0 = torch.from_numpy(p_h).cuda()
     tok = tok0.clone()
@@ -238,9 +248,9 @@ def main():
     def one_step():
         tok.copy_(tok0, non_blocking=True)
         p.copy_(p0, non_blocking=True)
-        dcl.dcl_denoise_step(run.model, tok, B, S, p, w.gen_end, kv, 0, stats, ws, ws_bytes, stream)
+        dcl.dcl_denoise_step(run.model, tok, B, S, p, w.gen_end, kv, score_flags, stats, ws, ws_bytes, stream)
         dcl.dcl_select_contiguous(tok, B, S, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id, stats,
-                                  k_raw, k_eff, 0, stream)
+                                  k_raw, k_eff, sel_flags, stream)
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
@@ -311,7 +321,8 @@ def main():
         max_steps = int(w.gen_end - p_h.min())
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        n_it = dcl.dcl_generate(run.model, tok, B, S, p, w.gen_end, kv, 0, w.window, w.tau_commit, w.tau_draft, 0,
+        n_it = dcl.dcl_generate(run.model, tok, B, S, p, w.gen_end, kv, score_flags, w.window, w.tau_commit,
+                                w.tau_draft, sel_flags,
                                 max_steps, 1, stats, k_raw, k_eff, hist, ws, ws_bytes, stream)
         torch.cuda.synchronize()
         t_gen = time.perf_counter() - t1
@@ -346,7 +357,8 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{w.key}: {w.description}", "geometry": g.name, "batch": B, "seq_len": S,
                    "kv_prefix": w.kv_prefix, "scored_rows": R, "window": w.window, "tau_commit": w.tau_commit,
-                   "tau_draft": w.tau_draft, "parallelism": "single GPU"},
+                   "tau_draft": w.tau_draft, "parallelism": "single GPU", "select": args.select,
+                   "score_all": bool(args.score_all), "suppress_mask": bool(args.suppress_mask)},
         "step_ms": {"median": round(float(np.median(step_ms)), 4), "p10": round(float(np.percentile(step_ms, 10)), 4),
                     "p90": round(float(np.percentile(step_ms, 90)), 4)},
         "gpu_sclk_mhz": clock,

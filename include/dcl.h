@@ -89,10 +89,15 @@ enum { DCL_DTYPE_F32 = 0, DCL_DTYPE_BF16 = 1 };
 
 /* dcl_denoise_step flags */
 #define DCL_SCORE_ALL_UNCOMMITTED 0x1u  /* score every position p <= i < gen_end, not only masks */
+#define DCL_SCORE_SUPPRESS_MASK 0x2u    /* leave the [MASK] id out of the vocabulary: it takes no
+                                           probability mass and is never top-1 or top-2 */
 /* dcl_select_contiguous flags */
 #define DCL_SEL_NO_PROGRESS_GUARD 0x1u  /* literal K: a step with K = 0 commits nothing */
 #define DCL_SEL_SCORE_ALL 0x2u          /* drafts may overwrite non-mask positions (pairs with
                                            DCL_SCORE_ALL_UNCOMMITTED) */
+#define DCL_SEL_NONCONTIGUOUS 0x4u      /* the independent threshold rule (Eq. threshold_pd) in the
+                                           window instead of Dynamic Contiguous Verification */
+#define DCL_SEL_CONTIGUOUS_DRAFTS 0x8u  /* drafts only along the leading chain (Appendix E) */
 
 /* Text for a status code; never NULL. */
 const char* dcl_status_string(dcl_status s);
@@ -148,7 +153,15 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
  *   x[p, min(p+L, gen_end)) = mask_id (Eq. remasking for the next iteration).
  * A window start whose row was not scored (top1 < 0) is never committed. Sequences with
  * p >= gen_end (or p < 0) are untouched (K_raw = K_eff = 0). K_raw, K_eff: device [B] outputs (may be
- * NULL). 1 <= L; 0 <= tau_commit <= 1; tau_draft >= 0 (values > 1 disable drafts). */
+ * NULL). 1 <= L; 0 <= tau_commit <= 1; tau_draft >= 0 (values > 1 disable drafts).
+ * DCL_SEL_CONTIGUOUS_DRAFTS (the variant of Appendix E): only the leading chain of the draft
+ *   region is drafted; it ends at the first eligible position (as above) with conf <= tau_draft,
+ *   and positions that already hold a token keep it without ending the chain.
+ * DCL_SEL_NONCONTIGUOUS (the baseline of Eq. threshold_pd, in the same window): every masked,
+ *   scored position j of [p, p + L_eff) with conf[j] > tau_commit is committed independently; if
+ *   none is and DCL_SEL_NO_PROGRESS_GUARD is off, the most confident one is (lowest j on ties);
+ *   p moves to the first position >= p still holding mask_id (gen_end if none); there are no
+ *   drafts and no remasking. K_raw = number above tau_commit, K_eff = number committed. */
 dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end,
                                  int32_t L, float tau_commit, float tau_draft, int32_t mask_id,
                                  dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,

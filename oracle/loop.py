@@ -7,7 +7,7 @@
 """
 import numpy as np
 
-from .select import select_contiguous
+from .select import noncontiguous_commit_set, select_contiguous  # noqa: F401
 from .step import step
 
 
@@ -55,7 +55,3 @@ def sequential_greedy(geom, weights, prompt, gen_len):
         x[:, i] = st["top1"][:, i]
     return x
 
-
-def noncontiguous_commit_set(conf_row: np.ndarray, lo: int, hi: int, tau: float):
-    """Eq. threshold_pd: positions i in [lo, hi) with max-probability c_i > tau."""
-    return {i for i in range(lo, hi) if conf_row[i] > tau}

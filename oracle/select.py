@@ -35,7 +35,7 @@ def compute_k(conf_window: np.ndarray, tau_commit: float) -> int:
 
 
 def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top1, conf,
-                      no_progress_guard=False, score_all=False):
+                      no_progress_guard=False, score_all=False, contiguous_drafts=False):
     """One selection step for every sequence: steps (iii)-(iv) of Section 3.3, then (i) for the next.
 
     tokens [B,S], p [B], top1/conf [B,S] (statistics of the forward on ``tokens``).
@@ -46,6 +46,9 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
       commit x[p : p + K_eff] = top1                                 (Algorithm 1, commit)
       for j in [p + L, gen_end): if (x_j = [MASK] or score_all) and conf_j > tau_draft:
           x_j = top1_j                                               (Eq. draft_update)
+        with contiguous_drafts (the variant of Appendix E): only the leading chain from p + L
+        is drafted: it ends at the first eligible position with conf <= tau_draft; positions
+        that already hold a token (not eligible) keep it and do not end the chain
       p += K_eff                                                     (Algorithm 1, advance)
       x[p : min(p + L, gen_end)] = [MASK]                            (Eq. remasking, next iteration)
     """
@@ -68,8 +71,50 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
             eligible = score_all or tokens[b, j] == mask_id
             if eligible and conf[b, j] > tau_draft:
                 x[b, j] = top1[b, j]
+            elif eligible and contiguous_drafts:
+                break                                     # the chain of Appendix E ends here
         pb += Ke
         pn[b] = pb
         for j in range(pb, min(pb + L, gen_end)):
             x[b, j] = mask_id
     return x, pn, K_raw, K_eff
+
+
+def select_noncontiguous(tokens, p, gen_end, L, tau, mask_id, top1, conf, no_progress_guard=False):
+    """The non-contiguous threshold rule (Eq. threshold_pd) inside the same sliding window.
+
+    Per sequence with p < gen_end, over the masked positions j of [p, p + L_eff):
+      commit x_j = top1_j for every such j with conf_j > tau (independent decisions, Eq. threshold_pd);
+      if none qualifies (and not no_progress_guard): commit the one with the highest confidence
+      (lowest position on ties) so the loop progresses;
+      p <- the first position >= p still holding [MASK] (gen_end if none): the verified prefix.
+    No drafts and no remasking: committed tokens past p stay committed.
+    Returns (new tokens, new p, K_raw = number passing tau, K_eff = number committed).
+    """
+    x = np.array(tokens, dtype=np.int64, copy=True)
+    pn = np.array(p, dtype=np.int64, copy=True)
+    B, S = x.shape
+    K_raw = np.zeros(B, np.int64)
+    K_eff = np.zeros(B, np.int64)
+    for b in range(B):
+        pb = int(pn[b])
+        if pb >= gen_end:
+            continue
+        hi = min(pb + L, gen_end)
+        cand = [j for j in range(pb, hi) if x[b, j] == mask_id and conf[b, j] >= 0]
+        passing = sorted(noncontiguous_commit_set(conf[b], pb, hi, tau) & set(cand))
+        commit = list(passing)
+        if not commit and cand and not no_progress_guard:
+            best = max(cand, key=lambda j: (conf[b, j], -j))
+            commit = [best]
+        for j in commit:
+            x[b, j] = top1[b, j]
+        K_raw[b], K_eff[b] = len(passing), len(commit)
+        masked = np.nonzero(x[b, pb:gen_end] == mask_id)[0]
+        pn[b] = pb + int(masked[0]) if len(masked) else gen_end
+    return x, pn, K_raw, K_eff
+
+
+def noncontiguous_commit_set(conf_row: np.ndarray, lo: int, hi: int, tau: float):
+    """Eq. threshold_pd: positions i in [lo, hi) with max-probability c_i > tau."""
+    return {i for i in range(lo, hi) if conf_row[i] > tau}

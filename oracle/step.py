@@ -12,7 +12,7 @@ from .select import scored_mask
 
 
 def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_boundary=True,
-         rope=True, return_logits_rows=None, dtype=np.float64, return_hidden=False):
+         rope=True, return_logits_rows=None, dtype=np.float64, return_hidden=False, suppress_mask=False):
     """Statistics dict with arrays [B, S]: top1, top2, conf, p2, lse.
 
     kv: optional callable (b, layer) -> (Kc [Hkv,P,dh], Vc [Hkv,dh,P]) with prefix length ``kv_prefix``
@@ -21,6 +21,7 @@ def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_bound
         (key "logits", [len, V]); they need not be scored rows.
     dtype: arithmetic of the evaluation (float64 = the oracle; float32 only sizes tolerances).
     return_hidden: also return the final hidden states h_f [B, S, d] (key "hidden").
+    suppress_mask: the [MASK] id is removed from the vocabulary of the statistics (``row_stats``).
     """
     tokens = np.asarray(tokens)
     B, S = tokens.shape
@@ -47,7 +48,8 @@ def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_bound
         if return_hidden:
             hidden[b] = hf
         if len(rows):
-            t1, t2, c, p2, lse = row_stats(lm_logits(weights, hf[rows], dtype=dtype))
+            t1, t2, c, p2, lse = row_stats(lm_logits(weights, hf[rows], dtype=dtype),
+                                           exclude=geom.mask_id if suppress_mask else None)
             out["top1"][b, rows] = t1
             out["top2"][b, rows] = t2
             out["conf"][b, rows] = c

@@ -11,8 +11,11 @@ from typing import Optional, Sequence
 HERE = os.path.dirname(os.path.abspath(__file__))
 DCL_DTYPE_F32, DCL_DTYPE_BF16 = 0, 1
 DCL_SCORE_ALL_UNCOMMITTED = 0x1
+DCL_SCORE_SUPPRESS_MASK = 0x2
 DCL_SEL_NO_PROGRESS_GUARD = 0x1
 DCL_SEL_SCORE_ALL = 0x2
+DCL_SEL_NONCONTIGUOUS = 0x4
+DCL_SEL_CONTIGUOUS_DRAFTS = 0x8
 STATUS = {0: "DCL_OK", 1: "DCL_E_ARG", 2: "DCL_E_UNSUPPORTED", 3: "DCL_E_WORKSPACE", 4: "DCL_E_HIP",
           5: "DCL_E_STATE"}
 

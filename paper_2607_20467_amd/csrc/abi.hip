@@ -290,7 +290,8 @@ dcl_status check_denoise_args(const Model* m, const int32_t* tokens, int32_t B, 
   if (st != DCL_OK) return st;
   if (!p) return fail(DCL_E_ARG, "p is NULL");
   if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
-  if (flags & ~(uint32_t)DCL_SCORE_ALL_UNCOMMITTED) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~(uint32_t)(DCL_SCORE_ALL_UNCOMMITTED | DCL_SCORE_SUPPRESS_MASK))
+    return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
   if (!out.top1 || !out.top2 || !out.conf || !out.p2 || !out.lse) return fail(DCL_E_ARG, "an output array is NULL");
   return DCL_OK;
 }
@@ -323,6 +324,7 @@ void enqueue_denoise(const Model* m, const int32_t* tokens, int32_t B, int32_t S
   lo.ps = at<float>(ws, L.ps);
   lo.n_vt = L.n_vt;
   lo.count = count;
+  lo.exclude = (flags & DCL_SCORE_SUPPRESS_MASK) ? c.mask_id : -1;
   {
     PROF(P_LM);
     gemm_lmhead(at<bf16_t>(m->wbuf, m->lay.lm), hf, c.vocab, L.T, c.d_model, lo, stream);
@@ -342,7 +344,11 @@ dcl_status check_select_args(const int32_t* tokens, int32_t B, int32_t S, const 
   if (L < 1) return fail(DCL_E_ARG, "window L=%d must be >= 1", L);
   if (!(tau_commit >= 0.f && tau_commit <= 1.f)) return fail(DCL_E_ARG, "tau_commit %g outside [0, 1]", tau_commit);
   if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
-  if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL)) return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL | DCL_SEL_NONCONTIGUOUS |
+                          DCL_SEL_CONTIGUOUS_DRAFTS))
+    return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
+  if ((flags & DCL_SEL_NONCONTIGUOUS) && (flags & (DCL_SEL_SCORE_ALL | DCL_SEL_CONTIGUOUS_DRAFTS)))
+    return fail(DCL_E_ARG, "DCL_SEL_NONCONTIGUOUS takes no draft or score-all flag (flags 0x%x)", flags);
   return DCL_OK;
 }
 

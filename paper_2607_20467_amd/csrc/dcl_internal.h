@@ -98,6 +98,7 @@ struct LmOut {
   int32_t *pi1, *pi2;
   int n_vt;
   const int32_t* count;  // number of valid X rows (device)
+  int exclude = -1;      // vocabulary id left out of the reduction (mask suppression), -1: none
 };
 // Tile shape / split-K choice for one GEMM shape (host).
 struct GemmPlan {

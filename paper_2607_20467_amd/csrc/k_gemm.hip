@@ -233,7 +233,7 @@ struct EpiLm {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int w = wq + 16 * i + r;
-          if (w < Nw) top2_push(p, acc[i][j][r], w);
+          if (w < Nw && w != o.exclude) top2_push(p, acc[i][j][r], w);
         }
 #pragma unroll
       for (int off = 16; off <= 32; off <<= 1) {
@@ -250,7 +250,7 @@ struct EpiLm {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int w = wq + 16 * i + r;
-          if (w < Nw) s += __expf(acc[i][j][r] - p.m1);
+          if (w < Nw && w != o.exclude) s += __expf(acc[i][j][r] - p.m1);
         }
       s += __shfl_xor(s, 16, 64);
       s += __shfl_xor(s, 32, 64);

@@ -304,6 +304,65 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
   const int L_eff = min(L, gen_end - pb);
   // window ends computed in 64-bit: p + L may exceed INT_MAX for a huge L
   const int draft_start = (int)min((long)pb + L, (long)gen_end);
+  if (flags & DCL_SEL_NONCONTIGUOUS) {
+    // Eq. threshold_pd in the window: independent commits of every masked, scored row above tau_c
+    __shared__ int npass[4];
+    __shared__ unsigned long long bestk[4];
+    int n = 0;
+    unsigned long long best = 0;  // (conf bits, ~j): max picks the highest conf, then the lowest j
+    for (int j = pb + tid; j < pb + L_eff; j += 256) {
+      if (x[j] == mask_id && top1[j] >= 0) {
+        const float c = conf[j];
+        if (c > tau_c) {
+          x[j] = top1[j];
+          ++n;
+        }
+        const unsigned long long k = ((unsigned long long)__float_as_uint(fmaxf(c, 0.f)) << 32) |
+                                     (unsigned long long)(0xFFFFFFFFu - (uint32_t)j);
+        best = k > best ? k : best;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      n += __shfl_xor(n, o, 64);
+      const unsigned long long v = __shfl_xor(best, o, 64);
+      best = v > best ? v : best;
+    }
+    if (lane == 0) {
+      npass[wid] = n;
+      bestk[wid] = best;
+    }
+    __syncthreads();
+    const int passing = (npass[0] + npass[1]) + (npass[2] + npass[3]);
+    unsigned long long bk = bestk[0];
+    for (int w = 1; w < 4; ++w) bk = bestk[w] > bk ? bestk[w] : bk;
+    int Ke = passing;
+    if (passing == 0 && bk != 0 && !(flags & DCL_SEL_NO_PROGRESS_GUARD)) {
+      const int jb = (int)(0xFFFFFFFFu - (uint32_t)(bk & 0xFFFFFFFFull));
+      if (tid == 0) x[jb] = top1[jb];
+      Ke = 1;
+    }
+    __syncthreads();
+    // p <- first position >= p still masked (the verified prefix ends there)
+    int firstm = gen_end;
+    for (int j = pb + tid; j < gen_end; j += 256)
+      if (x[j] == mask_id) {
+        firstm = j;
+        break;
+      }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) firstm = min(firstm, __shfl_xor(firstm, o, 64));
+    __syncthreads();
+    if (lane == 0) npass[wid] = firstm;
+    __syncthreads();
+    if (tid == 0) {
+      p[b] = min(min(npass[0], npass[1]), min(npass[2], npass[3]));
+      if (k_raw) k_raw[b] = passing;
+      if (k_eff) k_eff[b] = Ke;
+      if (k_hist) atomicAdd(&k_hist[Ke], 1);  // Ke <= L_eff <= L
+    }
+    return;
+  }
   // K = index of the first window row that fails conf > tau_c (Eq. compute_k), L_eff if none.
   int first = L_eff;
   for (int j = tid; j < L_eff; j += 256)
@@ -317,7 +376,21 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
   if (!(flags & DCL_SEL_NO_PROGRESS_GUARD) && Ke == 0 && top1[pb] >= 0) Ke = 1;
   for (int j = tid; j < Ke; j += 256) x[pb + j] = top1[pb + j];
   const bool any = (flags & DCL_SEL_SCORE_ALL) != 0;
-  for (int j = draft_start + tid; j < gen_end; j += 256)
+  int chain_end = gen_end;  // Appendix E: the draft chain ends at the first eligible row that fails
+  if (flags & DCL_SEL_CONTIGUOUS_DRAFTS) {
+    for (int j = draft_start + tid; j < gen_end; j += 256)
+      if ((any || x[j] == mask_id) && !(conf[j] > tau_d && top1[j] >= 0)) {
+        chain_end = j;
+        break;
+      }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) chain_end = min(chain_end, __shfl_xor(chain_end, o, 64));
+    __syncthreads();  // red[] is free again
+    if (lane == 0) red[wid] = chain_end;
+    __syncthreads();
+    chain_end = min(min(red[0], red[1]), min(red[2], red[3]));
+  }
+  for (int j = draft_start + tid; j < chain_end; j += 256)
     if ((any || x[j] == mask_id) && conf[j] > tau_d && top1[j] >= 0) x[j] = top1[j];
   __syncthreads();
   const int pn = pb + Ke;

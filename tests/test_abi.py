@@ -99,8 +99,11 @@ def test_step_and_select_argument_checks_without_gpu(dcl):
     assert sel(8, 1, 8, 8, 8, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # L = 0
     assert sel(8, 1, 8, 8, 8, 4, 1.5, 0.98, 3, st, None, None, 0, None) == 1      # tau_commit > 1
     assert sel(8, 1, 8, 8, 8, 4, 0.7, -0.1, 3, st, None, None, 0, None) == 1      # tau_draft < 0
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 8, None) == 1      # unknown flag
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 16, None) == 1     # unknown flag
     assert "flags" in dcl.dcl_last_error()
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 4 | 2, None) == 1  # non-contiguous + score-all
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 4 | 8, None) == 1  # non-contiguous + chain drafts
+    assert "NONCONTIGUOUS" in dcl.dcl_last_error()
     bad = dcl.binding.DclRowStats(0, 1, 0, 1, 1)
     assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, bad, None, None, 0, None) == 1
 
@@ -112,3 +115,14 @@ def test_product_has_no_oracle_dependency():
         if fn.endswith(".py"):
             src = open(os.path.join(pkg, fn)).read()
             assert not re.search(r"^\s*(import|from)\s+oracle", src, re.M), fn
+
+
+def test_binding_flag_constants_match_header():
+    """Every #define DCL_* flag of include/dcl.h has the same value in the Python binding."""
+    import paper_2607_20467_amd.binding as b
+    hdr = open(os.path.join(ROOT, "include", "dcl.h")).read()
+    defs = dict(re.findall(r"#define\s+(DCL_\w+)\s+(0x[0-9a-fA-F]+)u", hdr))
+    assert {"DCL_SCORE_ALL_UNCOMMITTED", "DCL_SCORE_SUPPRESS_MASK", "DCL_SEL_NONCONTIGUOUS",
+            "DCL_SEL_CONTIGUOUS_DRAFTS"} <= set(defs)
+    for name, val in defs.items():
+        assert getattr(b, name) == int(val, 16), name

@@ -62,3 +62,48 @@ def test_select_golden_cases():
                        c["tau_draft"], c["mask_id"], np.array([c["top1"]]), np.array([c["conf"]], np.float32))
         assert got[0][0].tolist() == c["expect_tokens"], c["name"]
         assert (got[1][0], got[2][0], got[3][0]) == (c["expect_p"], c["expect_K_raw"], c["expect_K_eff"]), c["name"]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_selection_variants_bit_exact(seed):
+    """DCL_SEL_NONCONTIGUOUS (Eq. threshold_pd in the window) and DCL_SEL_CONTIGUOUS_DRAFTS (Appendix E)
+    against the oracle's rules on random states, with exact threshold ties and confidence ties."""
+    import paper_2607_20467_amd as dcl
+    rng = np.random.default_rng(500 + seed)
+    mask = 4095
+    B, S = int(rng.integers(1, 9)), int(rng.integers(8, 700))
+    end = int(rng.integers(1, S + 1))
+    L = int(rng.choice([1, 2, 16, 32, 64, 128, 300]))
+    tok = rng.integers(0, 4000, (B, S))
+    p = rng.integers(0, end + 1, B)
+    p[0] = min(p[0], end - 1)
+    for b in range(B):
+        tok[b, p[b]:] = np.where(rng.random(S - p[b]) < 0.6, mask, tok[b, p[b]:])
+    NC, CD, NG, SA = dcl.DCL_SEL_NONCONTIGUOUS, dcl.DCL_SEL_CONTIGUOUS_DRAFTS, 1, 2
+    for flags in (NC, NC | NG, CD, CD | NG, CD | SA):
+        score_all = bool(flags & SA)
+        t = tok.copy()
+        if not flags & NC:
+            for b in range(B):
+                t[b, p[b]:min(p[b] + L, end)] = mask
+        sc = scored_mask(t, p, end, mask, score_all)
+        conf = np.where(sc, rng.uniform(0, 1, (B, S)).astype(np.float32), np.float32(-1)).astype(np.float32)
+        conf[sc & (rng.random((B, S)) < 0.05)] = np.float32(0.7)   # ties with tau_commit
+        conf[sc & (rng.random((B, S)) < 0.05)] = np.float32(0.25)  # ties between rows (non-contiguous guard)
+        if flags & CD:                                            # long passing runs so chains matter
+            for b in range(B):
+                lo = int(rng.integers(0, S))
+                hi = min(S, lo + int(rng.integers(1, 80)))
+                conf[b, lo:hi] = np.where(sc[b, lo:hi], np.float32(0.99), np.float32(-1))
+        top1 = np.where(sc, rng.integers(0, 4000, (B, S)), -1)
+        tc, td = np.float32(0.7), np.float32(rng.choice([0.3, 0.5, 0.9]))
+        if flags & NC:
+            ref = oracle.select_noncontiguous(t, p, end, L, float(tc), mask, top1, conf.astype(np.float64),
+                                              no_progress_guard=bool(flags & NG))
+        else:
+            ref = oracle.select_contiguous(t, p, end, L, float(tc), float(td), mask, top1, conf.astype(np.float64),
+                                           no_progress_guard=bool(flags & NG), score_all=score_all,
+                                           contiguous_drafts=True)
+        got = _run_gpu(t, p, end, L, float(tc), float(td), mask, top1, conf, flags)
+        for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
+            np.testing.assert_array_equal(g, r, err_msg=f"{name} flags={flags} B={B} S={S} L={L} end={end}")

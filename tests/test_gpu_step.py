@@ -201,3 +201,33 @@ def test_full_loop_matches_oracle_every_iteration():
         assert (p_host > p_before)[p_before < S].all()
         n += 1
     print("loop finished in", n, "iterations", flush=True)
+
+
+def test_mask_suppression_step():
+    """DCL_SCORE_SUPPRESS_MASK: the LM-head row of [MASK] is steered (through the oracle's own hidden
+    states) so that [MASK] would be the top-1 of every scored row; with the flag the statistics match
+    the oracle's softmax over the vocabulary without that id, and [MASK] is never top-1 or top-2."""
+    import paper_2607_20467_amd as dcl
+    w = CASES["c1"]
+    stored = dict(synth.make_weights(w.geom))
+    tok, p = synth.initial_state(w)
+    ref0 = oracle.step(w.geom, WeightView(stored), tok, p, w.gen_end, return_hidden=True)
+    sc = ref0["conf"] >= 0
+    hs = ref0["hidden"][sc]
+    d = (hs / np.linalg.norm(hs, axis=1, keepdims=True)).sum(0)
+    lm = stored["lm_head"].copy()
+    lm[w.geom.mask_id] = (d / np.linalg.norm(d) * np.linalg.norm(lm, axis=1).mean() * 3).astype(lm.dtype)
+    stored["lm_head"] = lm
+    W = WeightView(stored)
+    run = runner_for(w, stored)
+    plain = oracle.step(w.geom, W, tok, p, w.gen_end)
+    assert (plain["top1"][sc] == w.geom.mask_id).mean() > 0.9     # the steering worked
+    ref = oracle.step(w.geom, W, tok, p, w.gen_end, suppress_mask=True)
+    ct, lt = derived_tolerance(w.geom, W, tok, p, w.gen_end, ref, suppress_mask=True)
+    g = stats_to_np(run.step(to_dev(tok), to_dev(p), w.gen_end, flags=dcl.DCL_SCORE_SUPPRESS_MASK))
+    assert not (g["top1"][sc] == w.geom.mask_id).any() and not (g["top2"][sc] == w.geom.mask_id).any()
+    compare_stats(g, ref, what="suppress", conf_tol=ct, logit_tol=lt)
+    # and without the flag the GPU follows the unsuppressed oracle
+    ct0, lt0 = derived_tolerance(w.geom, W, tok, p, w.gen_end, plain)
+    compare_stats(stats_to_np(run.step(to_dev(tok), to_dev(p), w.gen_end)), plain, what="plain", conf_tol=ct0,
+                  logit_tol=lt0)

@@ -146,3 +146,96 @@ def test_contiguous_commits_subset_of_threshold_commits():
         tau = rng.uniform(0, 1)
         K = compute_k(conf[10:26], tau)
         assert set(range(10, 10 + K)) <= noncontiguous_commit_set(conf, 10, 26, tau)
+
+
+# ---------------------------------------------------------------- selection variants
+
+def test_row_stats_exclude_equals_vocabulary_without_that_id():
+    """Mask-id suppression: the statistics are those of the softmax over V with the id deleted."""
+    rng = np.random.default_rng(5)
+    l = rng.standard_normal((40, 97)) * 3
+    ex = 13
+    l[:20, ex] = l[:20].max(axis=1) + 2.0          # the excluded id would be the argmax in half the rows
+    t1, t2, c, p2, lse = oracle.row_stats(l, exclude=ex)
+    keep = np.array([v for v in range(97) if v != ex])
+    r1, r2, rc, rp2, rlse = oracle.row_stats(l[:, keep])
+    np.testing.assert_array_equal(t1, keep[r1])
+    np.testing.assert_array_equal(t2, keep[r2])
+    np.testing.assert_allclose(c, rc, rtol=1e-14)
+    np.testing.assert_allclose(p2, rp2, rtol=1e-14)
+    np.testing.assert_allclose(lse, rlse, rtol=1e-14)
+    assert not (t1 == ex).any() and not (t2 == ex).any()
+    # without the flag the argmax of the first rows is the (unsuppressed) id
+    assert (oracle.row_stats(l)[0][:20] == ex).all()
+
+
+def _state(S, p, mask, filled=()):
+    x = np.full((1, S), mask, np.int64)
+    x[0, :p] = 7
+    for j in filled:
+        x[0, j] = 9
+    return x, np.array([p])
+
+
+def test_noncontiguous_rule_by_hand():
+    mask, S, L = 99, 20, 6
+    x, p = _state(S, 4, mask, filled=(6,))          # position 6 already holds a token
+    conf = np.full((1, S), 0.2)
+    conf[0, [4, 5, 7, 8]] = [0.95, 0.1, 0.9, 0.85]
+    conf[0, 6] = -1.0                                # not scored (not masked)
+    top1 = np.arange(S)[None] + 1000
+    xn, pn, kr, ke = oracle.select_noncontiguous(x, p, S, L, 0.8, mask, top1, conf)
+    # window [4, 10): masked rows 4, 5, 7, 8, 9; passing > 0.8: 4, 7, 8 (independent decisions)
+    assert (kr[0], ke[0]) == (3, 3)
+    assert [int(v) for v in xn[0, 4:10]] == [1004, mask, 9, 1007, 1008, mask]
+    assert pn[0] == 5                                # first position still masked
+    # nothing passes: the most confident masked row is committed (lowest position on ties)
+    conf2 = np.full((1, S), 0.3)
+    conf2[0, 6] = -1.0
+    conf2[0, [7, 9]] = 0.5
+    xn, pn, kr, ke = oracle.select_noncontiguous(x, p, S, L, 0.8, mask, top1, conf2)
+    assert (kr[0], ke[0]) == (0, 1) and xn[0, 7] == 1007 and pn[0] == 4
+    xn, pn, kr, ke = oracle.select_noncontiguous(x, p, S, L, 0.8, mask, top1, conf2, no_progress_guard=True)
+    assert (kr[0], ke[0]) == (0, 0) and (xn == x).all() and pn[0] == 4
+
+
+def test_noncontiguous_equals_contiguous_when_the_passing_set_is_a_prefix():
+    """If the positions above the threshold form a leading run of the window (and every window row is
+    masked), the independent rule commits exactly what Eq. compute_k commits, and both advance p to
+    the end of that run (drafts off)."""
+    rng = np.random.default_rng(9)
+    mask, S, L, tau = 50, 40, 8, 0.7
+    for trial in range(200):
+        p0 = int(rng.integers(0, S - 1))
+        x, p = _state(S, p0, mask)
+        L_eff = min(L, S - p0)
+        K = int(rng.integers(1, L_eff + 1))
+        conf = rng.uniform(0.0, 0.7, (1, S))
+        conf[0, p0:p0 + K] = rng.uniform(0.71, 1.0, K)
+        top1 = rng.integers(0, 49, (1, S))
+        a = oracle.select_noncontiguous(x, p, S, L, tau, mask, top1, conf)
+        b = oracle.select_contiguous(x, p, S, L, tau, 2.0, mask, top1, conf)
+        np.testing.assert_array_equal(a[0], b[0])
+        np.testing.assert_array_equal(a[1], b[1])
+        assert a[2][0] == b[2][0] == K
+
+
+def test_contiguous_drafts_take_the_leading_chain():
+    mask, S, L = 99, 30, 4
+    x, p = _state(S, 2, mask, filled=(12,))         # an earlier draft at 12 (not masked, not scored)
+    conf = np.full((1, S), 0.1)
+    conf[0, 2:6] = 0.99                             # K = 4: p moves to 6 and [6, 10) is remasked afterwards
+    conf[0, 12] = -1.0
+    conf[0, [6, 7, 8, 9, 10, 11, 13, 14, 17, 18]] = 0.99   # chain from the old p + L = 6 breaks at 15
+    top1 = np.arange(S)[None] + 500
+    free = oracle.select_contiguous(x, p, S, L, 0.9, 0.95, mask, top1, conf)
+    chain = oracle.select_contiguous(x, p, S, L, 0.9, 0.95, mask, top1, conf, contiguous_drafts=True)
+    drafted = lambda r: [j for j in range(10, S) if r[0][0, j] not in (mask, 9)]
+    assert free[1][0] == chain[1][0] == 6
+    assert drafted(free) == [10, 11, 13, 14, 17, 18]
+    assert drafted(chain) == [10, 11, 13, 14]
+    # when every eligible draft row passes, the two rules agree
+    conf[0, [15, 16] + list(range(19, S))] = 0.99
+    a = oracle.select_contiguous(x, p, S, L, 0.9, 0.95, mask, top1, conf)
+    b = oracle.select_contiguous(x, p, S, L, 0.9, 0.95, mask, top1, conf, contiguous_drafts=True)
+    np.testing.assert_array_equal(a[0], b[0])
