@@ -65,14 +65,18 @@ typedef struct dcl_model_s* dcl_model_t;
 
 /* Per-position prediction statistics, each array [B, S] (row b*S + i), device memory.
  * Scored rows: top1 = argmax_v P(x_i = v), top2 = best other id (ties to the lowest id),
- * conf = P(top1) (the confidence c_i), p2 = P(top2), lse = log sum_v exp(logit_v).
- * Rows that are not scored: top1 = top2 = -1, conf = p2 = -1, lse = 0. */
+ * conf = P(top1) (the confidence c_i), p2 = P(top2), lse = log sum_v exp(logit_v),
+ * entropy = H(x_i) = -sum_v P log P = lse - sum_v P logit_v (the marginal entropy of the error
+ * bound in Section 2.2); conf - p2 is the top-1/top-2 margin.
+ * Rows that are not scored: top1 = top2 = -1, conf = p2 = -1, lse = 0, entropy = -1.
+ * entropy may be NULL (not written); the other arrays are required. */
 typedef struct {
   int32_t* top1;
   int32_t* top2;
   float* conf;
   float* p2;
   float* lse;
+  float* entropy;
 } dcl_row_stats;
 
 /* Cached prefix for the KV-cache step (dLLM-Cache combination, Section 4 "Scalability and
@@ -98,6 +102,8 @@ enum { DCL_DTYPE_F32 = 0, DCL_DTYPE_BF16 = 1 };
 #define DCL_SEL_NONCONTIGUOUS 0x4u      /* the independent threshold rule (Eq. threshold_pd) in the
                                            window instead of Dynamic Contiguous Verification */
 #define DCL_SEL_CONTIGUOUS_DRAFTS 0x8u  /* drafts only along the leading chain (Appendix E) */
+#define DCL_SEL_MARGIN 0x10u            /* accept on the margin conf - p2 instead of conf (commit
+                                           and draft thresholds alike) */
 
 /* Text for a status code; never NULL. */
 const char* dcl_status_string(dcl_status s);
@@ -161,7 +167,8 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
  *   scored position j of [p, p + L_eff) with conf[j] > tau_commit is committed independently; if
  *   none is and DCL_SEL_NO_PROGRESS_GUARD is off, the most confident one is (lowest j on ties);
  *   p moves to the first position >= p still holding mask_id (gen_end if none); there are no
- *   drafts and no remasking. K_raw = number above tau_commit, K_eff = number committed. */
+ *   drafts and no remasking. K_raw = number above tau_commit, K_eff = number committed.
+ * DCL_SEL_MARGIN: every comparison above uses conf - p2 (float32) in place of conf. */
 dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end,
                                  int32_t L, float tau_commit, float tau_draft, int32_t mask_id,
                                  dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,

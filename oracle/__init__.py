@@ -29,7 +29,7 @@ unpinned" against the paper itself.
 """
 from .numerics import bf16_round, rmsnorm, rope_tables, apply_rope, silu  # noqa: F401
 from .forward import forward, lm_logits  # noqa: F401
-from .scores import row_stats, SENTINEL_ID, SENTINEL_CONF  # noqa: F401
+from .scores import row_entropy, row_stats, SENTINEL_ID, SENTINEL_CONF  # noqa: F401
 from .select import compute_k, select_contiguous, select_noncontiguous, scored_mask  # noqa: F401
 from .step import step, step_from_weights  # noqa: F401
 from .loop import generate, sequential_greedy, noncontiguous_commit_set  # noqa: F401

@@ -39,3 +39,18 @@ def row_stats(logits: np.ndarray, exclude=None):
     p2 = P[np.arange(R), top2]
     lse = m + np.log(z)
     return top1, top2, conf, p2, lse
+
+
+def row_entropy(logits: np.ndarray, exclude=None):
+    """Entropy of each row's softmax, H = -sum_v P log P (Section 2.2: the marginal entropies H(x_i | C)
+    of the parallel-decoding error bound), over V without ``exclude`` if given. Natural log.
+    """
+    l = np.array(logits, dtype=np.float64, copy=True)
+    if exclude is not None:
+        l[:, int(exclude)] = -np.inf
+    m = l.max(axis=1, keepdims=True)
+    e = np.exp(l - m)
+    z = e.sum(axis=1, keepdims=True)
+    P = e / z
+    logP = np.where(P > 0, (l - m) - np.log(z), 0.0)
+    return -(P * logP).sum(axis=1)

@@ -7,7 +7,7 @@ top1/top2 = -1, conf/p2 = -1, lse = 0.
 import numpy as np
 
 from .forward import forward, lm_logits
-from .scores import SENTINEL_CONF, SENTINEL_ID, row_stats
+from .scores import SENTINEL_CONF, SENTINEL_ID, row_entropy, row_stats
 from .select import scored_mask
 
 
@@ -32,6 +32,7 @@ def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_bound
         "conf": np.full((B, S), SENTINEL_CONF),
         "p2": np.full((B, S), SENTINEL_CONF),
         "lse": np.zeros((B, S)),
+        "entropy": np.full((B, S), SENTINEL_CONF),
     }
     want = {} if return_logits_rows is None else {int(r): n for n, r in enumerate(return_logits_rows)}
     logits_out = None if return_logits_rows is None else np.empty((len(want), geom.vocab))
@@ -48,8 +49,10 @@ def step(geom, weights, tokens, p, gen_end, kv=None, score_all=False, bf16_bound
         if return_hidden:
             hidden[b] = hf
         if len(rows):
-            t1, t2, c, p2, lse = row_stats(lm_logits(weights, hf[rows], dtype=dtype),
-                                           exclude=geom.mask_id if suppress_mask else None)
+            lg = lm_logits(weights, hf[rows], dtype=dtype)
+            ex = geom.mask_id if suppress_mask else None
+            t1, t2, c, p2, lse = row_stats(lg, exclude=ex)
+            out["entropy"][b, rows] = row_entropy(lg, exclude=ex)
             out["top1"][b, rows] = t1
             out["top2"][b, rows] = t2
             out["conf"][b, rows] = c

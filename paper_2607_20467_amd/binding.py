@@ -16,6 +16,7 @@ DCL_SEL_NO_PROGRESS_GUARD = 0x1
 DCL_SEL_SCORE_ALL = 0x2
 DCL_SEL_NONCONTIGUOUS = 0x4
 DCL_SEL_CONTIGUOUS_DRAFTS = 0x8
+DCL_SEL_MARGIN = 0x10
 STATUS = {0: "DCL_OK", 1: "DCL_E_ARG", 2: "DCL_E_UNSUPPORTED", 3: "DCL_E_WORKSPACE", 4: "DCL_E_HIP",
           5: "DCL_E_STATE"}
 
@@ -35,7 +36,7 @@ class DclConfig(ctypes.Structure):
 
 class DclRowStats(ctypes.Structure):
     _fields_ = [("top1", ctypes.c_void_p), ("top2", ctypes.c_void_p), ("conf", ctypes.c_void_p),
-                ("p2", ctypes.c_void_p), ("lse", ctypes.c_void_p)]
+                ("p2", ctypes.c_void_p), ("lse", ctypes.c_void_p), ("entropy", ctypes.c_void_p)]
 
 
 PROF_CLASSES = ("embed", "rmsnorm", "gemm_qkv_rope", "attention", "gemm_o_residual", "gemm_gate_up_swiglu",
@@ -152,7 +153,8 @@ def dcl_workspace_bytes(model: int, B: int, S: int, kv_prefix: int = 0) -> int:
 
 
 def _stats(st) -> DclRowStats:
-    return DclRowStats(*(_ptr(st[k]) for k in ("top1", "top2", "conf", "p2", "lse")))
+    """st: dict of device arrays; "entropy" is optional (not written when absent)."""
+    return DclRowStats(*(_ptr(st.get(k)) for k in ("top1", "top2", "conf", "p2", "lse", "entropy")))
 
 
 def _kv(kv):
@@ -280,7 +282,8 @@ class Runner:
                 "top2": t.empty((B, S), dtype=t.int32, device="cuda"),
                 "conf": t.empty((B, S), dtype=t.float32, device="cuda"),
                 "p2": t.empty((B, S), dtype=t.float32, device="cuda"),
-                "lse": t.empty((B, S), dtype=t.float32, device="cuda")}
+                "lse": t.empty((B, S), dtype=t.float32, device="cuda"),
+                "entropy": t.empty((B, S), dtype=t.float32, device="cuda")}
 
     def step(self, tokens, p, gen_end, stats=None, kv=None, flags=0, stream=None):
         B, S = tokens.shape

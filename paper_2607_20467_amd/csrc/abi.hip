@@ -111,6 +111,7 @@ StepLayout step_layout(const dcl_config& c, int B, int S) {
   L.pm2 = take(np);
   L.pi2 = take(np);
   L.ps = take(np);
+  L.pt = take(np);
   // K-split slices of the residual GEMMs, folded into r by the next RMSNorm
   L.part = take((size_t)kMaxSplit * T * d * 4);
   L.total = off;
@@ -322,6 +323,7 @@ void enqueue_denoise(const Model* m, const int32_t* tokens, int32_t B, int32_t S
   lo.pm2 = at<float>(ws, L.pm2);
   lo.pi2 = at<int32_t>(ws, L.pi2);
   lo.ps = at<float>(ws, L.ps);
+  lo.pt = at<float>(ws, L.pt);
   lo.n_vt = L.n_vt;
   lo.count = count;
   lo.exclude = (flags & DCL_SCORE_SUPPRESS_MASK) ? c.mask_id : -1;
@@ -331,7 +333,7 @@ void enqueue_denoise(const Model* m, const int32_t* tokens, int32_t B, int32_t S
   }
   {
     PROF(P_MERGE);
-    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, L.T, out, stream);
+    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, lo.pt, L.n_vt, rows, count, L.T, out, stream);
   }
 }
 
@@ -339,13 +341,14 @@ dcl_status check_select_args(const int32_t* tokens, int32_t B, int32_t S, const 
                              int32_t L, float tau_commit, float tau_draft, const dcl_row_stats& in, uint32_t flags) {
   if (!tokens || !p) return fail(DCL_E_ARG, "tokens / p is NULL");
   if (!in.top1 || !in.conf) return fail(DCL_E_ARG, "in.top1 / in.conf is NULL");
+  if ((flags & DCL_SEL_MARGIN) && !in.p2) return fail(DCL_E_ARG, "DCL_SEL_MARGIN needs in.p2");
   if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
   if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
   if (L < 1) return fail(DCL_E_ARG, "window L=%d must be >= 1", L);
   if (!(tau_commit >= 0.f && tau_commit <= 1.f)) return fail(DCL_E_ARG, "tau_commit %g outside [0, 1]", tau_commit);
   if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
   if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL | DCL_SEL_NONCONTIGUOUS |
-                          DCL_SEL_CONTIGUOUS_DRAFTS))
+                          DCL_SEL_CONTIGUOUS_DRAFTS | DCL_SEL_MARGIN))
     return fail(DCL_E_ARG, "unknown flags 0x%x", flags);
   if ((flags & DCL_SEL_NONCONTIGUOUS) && (flags & (DCL_SEL_SCORE_ALL | DCL_SEL_CONTIGUOUS_DRAFTS)))
     return fail(DCL_E_ARG, "DCL_SEL_NONCONTIGUOUS takes no draft or score-all flag (flags 0x%x)", flags);
@@ -597,7 +600,7 @@ dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S
 }
 
 struct ScoreLayout {
-  size_t rows, count, pm1, pi1, pm2, pi2, ps, total;
+  size_t rows, count, pm1, pi1, pm2, pi2, ps, pt, total;
   int n_vt;
 };
 
@@ -618,6 +621,7 @@ static ScoreLayout score_layout(const dcl_config& c, int n) {
   L.pm2 = take(np);
   L.pi2 = take(np);
   L.ps = take(np);
+  L.pt = take(np);
   L.total = off;
   return L;
 }
@@ -652,6 +656,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   lo.pm2 = at<float>(ws, L.pm2);
   lo.pi2 = at<int32_t>(ws, L.pi2);
   lo.ps = at<float>(ws, L.ps);
+  lo.pt = at<float>(ws, L.pt);
   lo.n_vt = L.n_vt;
   lo.count = count;
   {
@@ -661,7 +666,7 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   }
   {
     PROF(P_MERGE);
-    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, L.n_vt, rows, count, n, out, stream);
+    launch_merge(lo.pm1, lo.pi1, lo.pm2, lo.pi2, lo.ps, lo.pt, L.n_vt, rows, count, n, out, stream);
   }
   return hip_check(hipGetLastError(), "score_hidden launch");
 }

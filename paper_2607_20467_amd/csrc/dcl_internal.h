@@ -55,7 +55,7 @@ struct Model {
 
 // Step workspace layout.
 struct StepLayout {
-  size_t r, u, q, k, vt, o, a, rows, count, hf, pm1, pi1, pm2, pi2, ps, part, total;
+  size_t r, u, q, k, vt, o, a, rows, count, hf, pm1, pi1, pm2, pi2, ps, pt, part, total;
   int T, S, Sp, n_vt;
 };
 
@@ -73,8 +73,8 @@ void launch_rmsnorm(float* r, const float* g, bf16_t* u, int T, int d, float eps
 void launch_compact(const int32_t* tokens, const int32_t* p, int B, int S, int gen_end, int mask_id,
                     int score_all, int32_t* rows, int32_t* count, dcl_row_stats st, hipStream_t s);
 void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const int32_t* pi2,
-                  const float* ps, int n_vt, const int32_t* rows, const int32_t* count, int max_rows,
-                  dcl_row_stats st, hipStream_t s);
+                  const float* ps, const float* pt, int n_vt, const int32_t* rows, const int32_t* count,
+                  int max_rows, dcl_row_stats st, hipStream_t s);
 void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s);
 void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c,
                    float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
@@ -95,6 +95,7 @@ struct QkvOut {
 };
 struct LmOut {
   float *pm1, *pm2, *ps;
+  float* pt;  // sum exp(l - m1) * (l - m1) per partial (entropy), relative like ps
   int32_t *pi1, *pi2;
   int n_vt;
   const int32_t* count;  // number of valid X rows (device)

@@ -184,7 +184,7 @@ __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 struct Part {
-  float m1, m2, s;
+  float m1, m2, s, t;  // s = sum exp(l - m1), t = sum exp(l - m1) (l - m1), both relative to m1
   int i1, i2;
 };
 constexpr size_t kLmEpiLds = sizeof(Part) * kLmWaves * 256;  // static LDS of the LM-head epilogue
@@ -204,10 +204,12 @@ __device__ __forceinline__ Part part_merge(const Part& a, const Part& b) {
     o.m1 = b.m1; o.i1 = b.i1;
     if (better(b.m2, b.i2, a.m1, a.i1)) { o.m2 = b.m2; o.i2 = b.i2; } else { o.m2 = a.m1; o.i2 = a.i1; }
   }
-  // sums are relative to each side's own top-1 value
-  const float sa = (a.m1 == -INFINITY) ? 0.f : a.s * __expf(a.m1 - o.m1);
-  const float sb = (b.m1 == -INFINITY) ? 0.f : b.s * __expf(b.m1 - o.m1);
-  o.s = sa + sb;
+  // sums are relative to each side's own top-1 value; moving t to the new reference m adds
+  // s (m1 - m) (each term exp(l - m1) (l - m1) becomes exp(l - m1) (l - m))
+  const float da = (a.m1 == -INFINITY) ? 0.f : a.m1 - o.m1, db = (b.m1 == -INFINITY) ? 0.f : b.m1 - o.m1;
+  const float ea = (a.m1 == -INFINITY) ? 0.f : __expf(da), eb = (b.m1 == -INFINITY) ? 0.f : __expf(db);
+  o.s = a.s * ea + b.s * eb;
+  o.t = ea * (a.t + a.s * da) + eb * (b.t + b.s * db);
   return o;
 }
 
@@ -227,7 +229,7 @@ struct EpiLm {
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
-      Part p = {-INFINITY, -INFINITY, 0.f, INT_MAX, INT_MAX};
+      Part p = {-INFINITY, -INFINITY, 0.f, 0.f, INT_MAX, INT_MAX};
 #pragma unroll
       for (int i = 0; i < SW; ++i)
 #pragma unroll
@@ -241,25 +243,35 @@ struct EpiLm {
         x.m1 = __shfl_xor(p.m1, off, 64); x.m2 = __shfl_xor(p.m2, off, 64);
         x.i1 = __shfl_xor(p.i1, off, 64); x.i2 = __shfl_xor(p.i2, off, 64);
         x.s = 0.f;
+        x.t = 0.f;
         Part y = part_merge(p, x);  // symmetric: ids differ, so argument order does not matter
         p.m1 = y.m1; p.m2 = y.m2; p.i1 = y.i1; p.i2 = y.i2;
       }
-      float s = 0.f;
+      float s = 0.f, t = 0.f;
 #pragma unroll
       for (int i = 0; i < SW; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int w = wq + 16 * i + r;
-          if (w < Nw && w != o.exclude) s += __expf(acc[i][j][r] - p.m1);
+          if (w < Nw && w != o.exclude) {
+            const float d = acc[i][j][r] - p.m1;
+            const float e = __expf(d);
+            s += e;
+            t += e * d;
+          }
         }
       s += __shfl_xor(s, 16, 64);
       s += __shfl_xor(s, 32, 64);
+      t += __shfl_xor(t, 16, 64);
+      t += __shfl_xor(t, 32, 64);
       p.s = s;
+      p.t = t;
       if (WW == 1) {
         const int t = tl + 16 * j;
         if (lane < 16 && t < R && t < T) {
           const size_t idx = (size_t)t * o.n_vt + tile_w;
           o.pm1[idx] = p.m1; o.pi1[idx] = p.i1; o.pm2[idx] = p.m2; o.pi2[idx] = p.i2; o.ps[idx] = p.s;
+          o.pt[idx] = p.t;
         }
       } else if (lane < 16) {
         xch[wave_w][(wave_t * ST + j) * 16 + lane] = p;
@@ -277,6 +289,7 @@ struct EpiLm {
             for (int v = 1; v < WW; ++v) p = part_merge(p, xch[v][(wave_t * ST + j) * 16 + lane]);
             const size_t idx = (size_t)t * o.n_vt + tile_w;
             o.pm1[idx] = p.m1; o.pi1[idx] = p.i1; o.pm2[idx] = p.m2; o.pi2[idx] = p.i2; o.ps[idx] = p.s;
+            o.pt[idx] = p.t;
           }
         }
       }

@@ -178,6 +178,7 @@ __global__ void __launch_bounds__(1024) compact_kernel(const int32_t* __restrict
         st.conf[idx] = -1.f;
         st.p2[idx] = -1.f;
         st.lse[idx] = 0.f;
+        if (st.entropy) st.entropy[idx] = -1.f;
       }
     }
     unsigned long long m = __ballot(flag);
@@ -230,8 +231,8 @@ __device__ __forceinline__ Top2 top2_merge(Top2 a, Top2 b) {
 // conf = 1 / S, p2 = exp(m2 - M) / S, lse = M + log S with M = global max, S = sum_t s_t e^(m1_t - M).
 __global__ void __launch_bounds__(256) merge_kernel(const float* __restrict__ pm1, const int32_t* __restrict__ pi1,
                                                    const float* __restrict__ pm2, const int32_t* __restrict__ pi2,
-                                                   const float* __restrict__ ps, int n_vt,
-                                                   const int32_t* __restrict__ rows,
+                                                   const float* __restrict__ ps, const float* __restrict__ pt,
+                                                   int n_vt, const int32_t* __restrict__ rows,
                                                    const int32_t* __restrict__ count, dcl_row_stats st) {
   int lane = threadIdx.x & 63;
   int j = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -248,10 +249,20 @@ __global__ void __launch_bounds__(256) merge_kernel(const float* __restrict__ pm
     t = top2_merge(t, x);  // symmetric (distinct ids), so every lane computes the same result
   }
   const float M = t.m1;
-  float s = 0.f;
-  for (int v = lane; v < n_vt; v += 64) s += ps[base + v] * __expf(pm1[base + v] - M);
+  // S = sum_v exp(l_v - M), Tm = sum_v exp(l_v - M) (l_v - M) from the tiles' relative sums
+  float s = 0.f, tm = 0.f;
+  for (int v = lane; v < n_vt; v += 64) {
+    const float m = pm1[base + v];
+    if (m == -INFINITY) continue;  // a tile with no ids left
+    const float d = m - M, e = __expf(d), sv = ps[base + v];
+    s += sv * e;
+    tm += e * (pt[base + v] + sv * d);
+  }
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  for (int o = 32; o >= 1; o >>= 1) {
+    s += __shfl_xor(s, o, 64);
+    tm += __shfl_xor(tm, o, 64);
+  }
   if (lane == 0) {
     int row = rows[j];
     st.top1[row] = t.i1;
@@ -259,14 +270,15 @@ __global__ void __launch_bounds__(256) merge_kernel(const float* __restrict__ pm
     st.conf[row] = 1.0f / s;
     st.p2[row] = __expf(t.m2 - M) / s;
     st.lse[row] = M + logf(s);
+    if (st.entropy) st.entropy[row] = logf(s) - tm / s;  // H = log S - Tm / S
   }
 }
 
 void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const int32_t* pi2, const float* ps,
-                  int n_vt, const int32_t* rows, const int32_t* count, int max_rows, dcl_row_stats st,
-                  hipStream_t s) {
+                  const float* pt, int n_vt, const int32_t* rows, const int32_t* count, int max_rows,
+                  dcl_row_stats st, hipStream_t s) {
   if (max_rows == 0) return;
-  hipLaunchKernelGGL(merge_kernel, dim3((max_rows + 3) / 4), dim3(256), 0, s, pm1, pi1, pm2, pi2, ps, n_vt, rows,
+  hipLaunchKernelGGL(merge_kernel, dim3((max_rows + 3) / 4), dim3(256), 0, s, pm1, pi1, pm2, pi2, ps, pt, n_vt, rows,
                      count, st);
 }
 
@@ -292,7 +304,11 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   int32_t* x = tokens + (size_t)b * S;
   const int32_t* top1 = st.top1 + (size_t)b * S;
-  const float* conf = st.conf + (size_t)b * S;
+  const float* cf = st.conf + (size_t)b * S;
+  const float* p2 = st.p2 + (size_t)b * S;
+  const bool margin = (flags & DCL_SEL_MARGIN) != 0;
+  // the acceptance statistic: the confidence, or the top-1/top-2 margin (unscored rows stay -1)
+  auto conf_at = [&](int j) -> float { return (margin && cf[j] >= 0.f) ? cf[j] - p2[j] : cf[j]; };
   const int pb = p[b];
   if (pb < 0 || pb >= gen_end) {  // finished (or invalid) pointer: the sequence is left untouched
     if (tid == 0) {
@@ -312,7 +328,7 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
     unsigned long long best = 0;  // (conf bits, ~j): max picks the highest conf, then the lowest j
     for (int j = pb + tid; j < pb + L_eff; j += 256) {
       if (x[j] == mask_id && top1[j] >= 0) {
-        const float c = conf[j];
+        const float c = conf_at(j);
         if (c > tau_c) {
           x[j] = top1[j];
           ++n;
@@ -366,7 +382,7 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
   // K = index of the first window row that fails conf > tau_c (Eq. compute_k), L_eff if none.
   int first = L_eff;
   for (int j = tid; j < L_eff; j += 256)
-    if (!(conf[pb + j] > tau_c)) first = min(first, j);
+    if (!(conf_at(pb + j) > tau_c)) first = min(first, j);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
   if (lane == 0) red[wid] = first;
@@ -379,7 +395,7 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
   int chain_end = gen_end;  // Appendix E: the draft chain ends at the first eligible row that fails
   if (flags & DCL_SEL_CONTIGUOUS_DRAFTS) {
     for (int j = draft_start + tid; j < gen_end; j += 256)
-      if ((any || x[j] == mask_id) && !(conf[j] > tau_d && top1[j] >= 0)) {
+      if ((any || x[j] == mask_id) && !(conf_at(j) > tau_d && top1[j] >= 0)) {
         chain_end = j;
         break;
       }
@@ -391,7 +407,7 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
     chain_end = min(min(red[0], red[1]), min(red[2], red[3]));
   }
   for (int j = draft_start + tid; j < chain_end; j += 256)
-    if ((any || x[j] == mask_id) && conf[j] > tau_d && top1[j] >= 0) x[j] = top1[j];
+    if ((any || x[j] == mask_id) && conf_at(j) > tau_d && top1[j] >= 0) x[j] = top1[j];
   __syncthreads();
   const int pn = pb + Ke;
   const int stop = (int)min((long)pn + L, (long)gen_end);

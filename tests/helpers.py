@@ -65,8 +65,12 @@ def derived_tolerance(geom, W, tok, p, gen_end, ref, **step_kw):
     return tol
 
 
-def compare_stats(gpu, ref, tau_c=None, tau_d=None, what="", conf_tol=CONF_TOL, logit_tol=LOGIT_TOL):
-    """Parity of one step's statistics against the oracle. Returns a report dict; asserts the bar."""
+def compare_stats(gpu, ref, tau_c=None, tau_d=None, what="", conf_tol=CONF_TOL, logit_tol=LOGIT_TOL,
+                  entropy_tol=None):
+    """Parity of one step's statistics against the oracle. Returns a report dict; asserts the bar.
+    Entropy (when both sides have it): H = lse - E_P[logit] moves by at most twice the logit
+    tolerance when every logit moves by at most that much (both terms are P-weighted averages of
+    the logit changes), so the default bar is 2 x logit_tol."""
     scored = ref["conf"] >= 0
     np.testing.assert_array_equal(gpu["conf"] >= 0, scored, err_msg=f"{what}: scored-row sets differ")
     np.testing.assert_array_equal(gpu["top1"][~scored], -1)
@@ -84,6 +88,12 @@ def compare_stats(gpu, ref, tau_c=None, tau_d=None, what="", conf_tol=CONF_TOL, 
            "near_tie_rows": int(tie.sum()), "near_threshold_rows": int(near.sum()),
            "meets_exact_input_bar": bool((dc.size == 0 or dc.max() <= CONF_TOL) and not (mism & ~(
                _gap(ref, scored) < TIE_GAP)).any())}
+    if "entropy" in gpu and "entropy" in ref:
+        np.testing.assert_array_equal(gpu["entropy"][~scored], -1.0)
+        dh = np.abs(gpu["entropy"][scored] - ref["entropy"][scored])
+        rep["entropy_max_abs"] = float(dh.max()) if dh.size else 0.0
+        et = 2 * logit_tol if entropy_tol is None else entropy_tol
+        assert dh.size == 0 or (dh <= et).all(), f"{what}: entropy max-abs {dh.max():.3g} > {np.min(et):.3g}"
     print(what, rep, flush=True)
     assert dc.size == 0 or dc.max() <= conf_tol, f"{what}: conf max-abs {dc.max():.3g} > {conf_tol:.3g}"
     assert dl.size == 0 or dl.max() <= logit_tol, f"{what}: lse max-abs {dl.max():.3g} > {logit_tol:.3g}"

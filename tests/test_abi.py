@@ -99,7 +99,7 @@ def test_step_and_select_argument_checks_without_gpu(dcl):
     assert sel(8, 1, 8, 8, 8, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # L = 0
     assert sel(8, 1, 8, 8, 8, 4, 1.5, 0.98, 3, st, None, None, 0, None) == 1      # tau_commit > 1
     assert sel(8, 1, 8, 8, 8, 4, 0.7, -0.1, 3, st, None, None, 0, None) == 1      # tau_draft < 0
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 16, None) == 1     # unknown flag
+    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 64, None) == 1     # unknown flag
     assert "flags" in dcl.dcl_last_error()
     assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 4 | 2, None) == 1  # non-contiguous + score-all
     assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 4 | 8, None) == 1  # non-contiguous + chain drafts

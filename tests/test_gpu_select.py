@@ -8,7 +8,7 @@ from oracle.select import scored_mask
 pytestmark = pytest.mark.gpu
 
 
-def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0):
+def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0, p2=None):
     import torch
     import paper_2607_20467_amd as dcl
     B, S = tok.shape
@@ -17,7 +17,7 @@ def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0):
     st = {"top1": torch.from_numpy(top1.astype(np.int32)).cuda(),
           "top2": torch.zeros((B, S), dtype=torch.int32, device="cuda"),
           "conf": torch.from_numpy(conf.astype(np.float32)).cuda(),
-          "p2": torch.zeros((B, S), dtype=torch.float32, device="cuda"),
+          "p2": (torch.zeros((B, S), dtype=torch.float32) if p2 is None else torch.from_numpy(p2.astype(np.float32))).cuda(),
           "lse": torch.zeros((B, S), dtype=torch.float32, device="cuda")}
     kr = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     ke = torch.full((B,), -7, dtype=torch.int32, device="cuda")
@@ -105,5 +105,47 @@ def test_selection_variants_bit_exact(seed):
                                            no_progress_guard=bool(flags & NG), score_all=score_all,
                                            contiguous_drafts=True)
         got = _run_gpu(t, p, end, L, float(tc), float(td), mask, top1, conf, flags)
+        for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
+            np.testing.assert_array_equal(g, r, err_msg=f"{name} flags={flags} B={B} S={S} L={L} end={end}")
+
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_margin_acceptance_bit_exact(seed):
+    """DCL_SEL_MARGIN: every rule applied to the float32 margin conf - p2 (unscored rows -1) equals the
+    oracle's rule applied to the same float32 values."""
+    import paper_2607_20467_amd as dcl
+    rng = np.random.default_rng(900 + seed)
+    mask = 4095
+    B, S = int(rng.integers(1, 6)), int(rng.integers(8, 500))
+    end = int(rng.integers(1, S + 1))
+    L = int(rng.choice([1, 16, 32, 100]))
+    tok = rng.integers(0, 4000, (B, S))
+    p = rng.integers(0, end + 1, B)
+    p[0] = min(p[0], end - 1)
+    for b in range(B):
+        tok[b, p[b]:] = np.where(rng.random(S - p[b]) < 0.6, mask, tok[b, p[b]:])
+    MG = dcl.DCL_SEL_MARGIN
+    for flags in (MG, MG | dcl.DCL_SEL_CONTIGUOUS_DRAFTS, MG | dcl.DCL_SEL_NONCONTIGUOUS):
+        t = tok.copy()
+        if not flags & dcl.DCL_SEL_NONCONTIGUOUS:
+            for b in range(B):
+                t[b, p[b]:min(p[b] + L, end)] = mask
+        sc = scored_mask(t, p, end, mask)
+        c = rng.uniform(0.3, 1.0, (B, S)).astype(np.float32)
+        q = (c * rng.uniform(0, 1, (B, S))).astype(np.float32)          # p2 <= conf
+        q[rng.random((B, S)) < 0.05] = np.float32(0.1)
+        c[rng.random((B, S)) < 0.05] = np.float32(0.6)                 # margin ties with tau: 0.6 - 0.1 = 0.5
+        conf = np.where(sc, c, np.float32(-1)).astype(np.float32)
+        p2 = np.where(sc, q, np.float32(-1)).astype(np.float32)
+        marg = np.where(sc, (conf - p2).astype(np.float32), np.float32(-1)).astype(np.float64)
+        top1 = np.where(sc, rng.integers(0, 4000, (B, S)), -1)
+        tc, td = 0.5, float(np.float32(rng.choice([0.3, 0.5, 0.8])))
+        if flags & dcl.DCL_SEL_NONCONTIGUOUS:
+            ref = oracle.select_noncontiguous(t, p, end, L, tc, mask, top1, marg)
+        else:
+            ref = oracle.select_contiguous(t, p, end, L, tc, td, mask, top1, marg,
+                                           contiguous_drafts=bool(flags & dcl.DCL_SEL_CONTIGUOUS_DRAFTS))
+        got = _run_gpu(t, p, end, L, tc, td, mask, top1, conf, flags, p2=p2)
         for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
             np.testing.assert_array_equal(g, r, err_msg=f"{name} flags={flags} B={B} S={S} L={L} end={end}")

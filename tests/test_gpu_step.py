@@ -99,10 +99,15 @@ def test_score_hidden_exact_bar(key):
     n = 203
     h = synth.normal_bf16(77, 0, 1.0, (n, w.geom.d_model))
     st = stats_to_np(run.score_hidden(torch.from_numpy(h.view(np.int16)).cuda()))
-    t1, t2, c, p2, lse = oracle.row_stats(oracle.lm_logits(W, synth.bf16_bits_to_f32(h).astype(np.float64)))
-    ref = {"top1": t1[None], "top2": t2[None], "conf": c[None], "p2": p2[None], "lse": lse[None]}
+    lg = oracle.lm_logits(W, synth.bf16_bits_to_f32(h).astype(np.float64))
+    t1, t2, c, p2, lse = oracle.row_stats(lg)
+    H = oracle.row_entropy(lg)
+    ref = {"top1": t1[None], "top2": t2[None], "conf": c[None], "p2": p2[None], "lse": lse[None], "entropy": H[None]}
     gpu = {k: v[None] for k, v in st.items()}
-    rep = compare_stats(gpu, ref, what=f"score_hidden[{key}]")
+    # entropy bar per row: dH/dl_v = -P_v (l_v - E_P l), so |dH| <= max|dl| * E_P|l - E_P l| <= max|dl| * sd_P(l)
+    P = np.exp(lg - lse[:, None])
+    sd = np.sqrt(np.maximum((P * lg ** 2).sum(1) - (P * lg).sum(1) ** 2, 0.0))
+    rep = compare_stats(gpu, ref, what=f"score_hidden[{key}]", entropy_tol=(LOGIT_TOL * np.maximum(sd, 1.0))[None])
     assert rep["meets_exact_input_bar"]
     np.testing.assert_allclose(st["p2"], p2, atol=CONF_TOL)
     gap = np.log(c) - np.log(p2)
@@ -231,3 +236,22 @@ def test_mask_suppression_step():
     ct0, lt0 = derived_tolerance(w.geom, W, tok, p, w.gen_end, plain)
     compare_stats(stats_to_np(run.step(to_dev(tok), to_dev(p), w.gen_end)), plain, what="plain", conf_tol=ct0,
                   logit_tol=lt0)
+
+
+def test_entropy_of_steered_and_flat_rows():
+    """Entropy through the fused reduction at its extremes: a hidden row aligned with one LM-head row
+    (near one-hot, H -> 0) and the zero hidden row (uniform softmax, H = log V exactly)."""
+    import torch
+    w, stored, W, run = _setup("c1")
+    V, d = w.geom.vocab, w.geom.d_model
+    lm = np.asarray(stored["lm_head"], np.float32)
+    h = np.zeros((2, d), np.float32)
+    h[0] = lm[17] / np.linalg.norm(lm[17]) * 8.0
+    hb = torch.from_numpy(h).to(torch.bfloat16)
+    st = stats_to_np(run.score_hidden(hb.view(torch.int16).cuda()))
+    lg = oracle.lm_logits(W, hb.float().numpy().astype(np.float64))
+    H = oracle.row_entropy(lg)
+    print("entropy: steered row", st["entropy"][0], "oracle", H[0], "| zero row", st["entropy"][1], "log V", np.log(V))
+    assert H[1] == pytest.approx(np.log(V), rel=1e-12)
+    assert abs(st["entropy"][1] - np.log(V)) < 1e-4
+    assert abs(st["entropy"][0] - H[0]) < 2 * LOGIT_TOL

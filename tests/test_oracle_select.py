@@ -239,3 +239,19 @@ def test_contiguous_drafts_take_the_leading_chain():
     a = oracle.select_contiguous(x, p, S, L, 0.9, 0.95, mask, top1, conf)
     b = oracle.select_contiguous(x, p, S, L, 0.9, 0.95, mask, top1, conf, contiguous_drafts=True)
     np.testing.assert_array_equal(a[0], b[0])
+
+
+def test_row_entropy_against_scipy_and_extremes():
+    import scipy.stats
+    rng = np.random.default_rng(3)
+    l = rng.standard_normal((30, 200)) * 5
+    H = oracle.row_entropy(l)
+    np.testing.assert_allclose(H, scipy.stats.entropy(scipy.special.softmax(l, axis=1), axis=1), rtol=1e-12)
+    assert oracle.row_entropy(np.zeros((1, 77)))[0] == pytest.approx(np.log(77), rel=1e-14)   # uniform
+    one = np.full((1, 50), -np.inf)
+    one[0, 3] = 2.0
+    assert oracle.row_entropy(one)[0] == 0.0                                                   # one-hot
+    # the excluded id: entropy of the vocabulary without it
+    keep = [v for v in range(200) if v != 11]
+    np.testing.assert_allclose(oracle.row_entropy(l, exclude=11), oracle.row_entropy(l[:, keep]), rtol=1e-13)
+    assert (H <= np.log(200) + 1e-12).all() and (H >= 0).all()
