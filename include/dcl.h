@@ -80,13 +80,16 @@ typedef struct {
 } dcl_row_stats;
 
 /* Cached prefix for the KV-cache step (dLLM-Cache combination, Section 4 "Scalability and
- * Extension"): per layer l, k[l] -> bf16 [B, n_kv_heads, prefix_len, head_dim] keys AFTER RoPE,
- * v[l] -> bf16 [B, n_kv_heads, head_dim, prefix_len] values (key index contiguous).
- * `k` and `v` themselves are HOST arrays of n_layers device pointers. prefix_len % 8 == 0. */
+ * Extension"): per layer l, k[l] -> bf16 [B, n_kv_heads, capacity, head_dim] keys AFTER RoPE,
+ * v[l] -> bf16 [B, n_kv_heads, head_dim, capacity] values (key index contiguous); positions
+ * [0, prefix_len) are in use. capacity = 0 means capacity = prefix_len.
+ * `k` and `v` themselves are HOST arrays of n_layers device pointers (writable buffers for
+ * dcl_kv_append). prefix_len % 8 == 0, capacity % 8 == 0, prefix_len <= capacity. */
 typedef struct {
   const void* const* k;
   const void* const* v;
   int32_t prefix_len;
+  int32_t capacity;
 } dcl_kv;
 
 enum { DCL_DTYPE_F32 = 0, DCL_DTYPE_BF16 = 1 };
@@ -195,6 +198,18 @@ dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S
                         int32_t check_every, dcl_row_stats stats, int32_t* K_raw, int32_t* K_eff,
                         int32_t* k_hist, void* ws, size_t ws_bytes, int32_t* steps_out,
                         hipStream_t stream);
+
+/* KV-cache write-back (the cache maintenance of the dLLM-Cache combination, Section 4): the forward
+ * of the S tokens [B, S] (device) at positions prefix_len + i over the cached prefix `kv`, as in
+ * dcl_denoise_step, writing every layer's keys (after RoPE) and values of those tokens into the
+ * cache at positions [prefix_len, prefix_len + S). The caller then uses prefix_len + S (for
+ * example after the block's tokens are committed). With prefix_len = 0 over a whole sequence it
+ * is the periodic refresh: every cached position is recomputed with the full context. No LM head
+ * runs; the last layer stops after its keys and values. Needs prefix_len + S <= capacity and a
+ * workspace of dcl_workspace_bytes(model, B, S, prefix_len) bytes; the cache is read at positions
+ * [0, prefix_len) and written at [prefix_len, prefix_len + S). */
+dcl_status dcl_kv_append(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
+                         const dcl_kv* kv, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Workspace bytes for dcl_score_hidden over n rows; 0 if the arguments are invalid. */
 size_t dcl_score_workspace_bytes(dcl_model_t model, int32_t n);

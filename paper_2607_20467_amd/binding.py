@@ -49,7 +49,7 @@ class DclProfile(ctypes.Structure):
 
 class DclKV(ctypes.Structure):
     _fields_ = [("k", ctypes.POINTER(ctypes.c_void_p)), ("v", ctypes.POINTER(ctypes.c_void_p)),
-                ("prefix_len", ctypes.c_int32)]
+                ("prefix_len", ctypes.c_int32), ("capacity", ctypes.c_int32)]
 
 
 def library_path() -> str:
@@ -84,6 +84,7 @@ def load_library():
         "dcl_generate": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, i32, f32, f32, u32,
                                         i32, i32, DclRowStats, vp, vp, vp, vp, sz, ctypes.POINTER(i32), vp]),
         "dcl_score_workspace_bytes": (sz, [vp, i32]),
+        "dcl_kv_append": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, sz, vp]),
         "dcl_profile_enable": (ctypes.c_int, [i32]),
         "dcl_profile_read": (ctypes.c_int, [ctypes.POINTER(DclProfile)]),
         "dcl_score_hidden": (ctypes.c_int, [vp, vp, i32, DclRowStats, vp, sz, vp]),
@@ -158,13 +159,15 @@ def _stats(st) -> DclRowStats:
 
 
 def _kv(kv):
-    """kv: None or (list of per-layer K tensors, list of per-layer V tensors, prefix_len)."""
+    """kv: None or (per-layer K tensors, per-layer V tensors, prefix_len[, capacity])."""
     if kv is None:
         return None, None
-    ks, vs, P = kv
+    ks, vs, P = kv[:3]
+    cap = kv[3] if len(kv) > 3 else 0
     ka = (ctypes.c_void_p * len(ks))(*[_ptr(t) for t in ks])
     va = (ctypes.c_void_p * len(vs))(*[_ptr(t) for t in vs])
-    s = DclKV(ctypes.cast(ka, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(va, ctypes.POINTER(ctypes.c_void_p)), P)
+    s = DclKV(ctypes.cast(ka, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(va, ctypes.POINTER(ctypes.c_void_p)), P,
+              cap)
     return ctypes.byref(s), (s, ka, va)
 
 
@@ -195,6 +198,13 @@ def dcl_generate(model: int, tokens, B: int, S: int, p, gen_end: int, kv, score_
                                        _stream(stream)), "dcl_generate")
     del keep
     return steps.value
+
+
+def dcl_kv_append(model: int, tokens, B: int, S: int, kv, ws, ws_bytes: int, stream=None) -> None:
+    kvp, keep = _kv(kv)
+    _check(load_library().dcl_kv_append(model, _ptr(tokens), B, S, kvp, _ptr(ws), ws_bytes, _stream(stream)),
+           "dcl_kv_append")
+    del keep
 
 
 def dcl_profile_enable(on: bool) -> None:
@@ -302,6 +312,12 @@ class Runner:
             if with_hidden else None
         dcl_debug_logits(self.model, tokens, B, S, kv, rows, rows.numel(), out, hid, ws, n, stream)
         return (out, hid) if with_hidden else out
+
+    def kv_append(self, tokens, kv, stream=None):
+        """Write the keys/values of tokens [B, S] at positions kv[2] + i into the cache kv (see dcl_kv_append)."""
+        B, S = tokens.shape
+        ws, n = self.workspace(B, S, kv[2])
+        dcl_kv_append(self.model, tokens, B, S, kv, ws, n, stream)
 
     def score_hidden(self, hidden, stream=None):
         """Statistics of given bf16 hidden rows (int16 bit patterns or torch.bfloat16, [n, d])."""

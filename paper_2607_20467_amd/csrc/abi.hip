@@ -193,6 +193,9 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   if (kv) {
     if (!kv->k || !kv->v) return fail(DCL_E_ARG, "kv->k / kv->v is NULL");
     if (P < 0 || P % 8 != 0) return fail(DCL_E_UNSUPPORTED, "kv prefix_len %d must be a non-negative multiple of 8", P);
+    const int cap = kv->capacity ? kv->capacity : P;
+    if (cap < P || cap % 8 != 0)
+      return fail(DCL_E_ARG, "kv capacity %d must be a multiple of 8 and >= prefix_len %d", kv->capacity, P);
     for (int l = 0; l < m->cfg.n_layers; ++l)
       if (P > 0 && (!kv->k[l] || !kv->v[l])) return fail(DCL_E_ARG, "kv cache pointer of layer %d is NULL", l);
   }
@@ -208,7 +211,7 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
 // a2-a7: embedding and every transformer layer. Returns the number of K-split slices of the last
 // residual GEMM still to be added to ws.r (the final RMSNorm folds them in).
 int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_kv* kv, void* ws,
-                 const StepLayout& L, hipStream_t s) {
+                 const StepLayout& L, hipStream_t s, bool writeback = false) {
   const dcl_config& c = m->cfg;
   const int T = B * S, d = c.d_model, dh = c.head_dim;
   const int P = kv ? kv->prefix_len : 0;
@@ -245,6 +248,12 @@ int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_k
       PROF(P_QKV);
       gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
     }
+    if (writeback) {  // this layer's fresh keys and values into the cache at [P, P + S)
+      launch_kv_writeback(qo.k, qo.vt, static_cast<bf16_t*>(const_cast<void*>(kv->k[l])),
+                          static_cast<bf16_t*>(const_cast<void*>(kv->v[l])), B, c.n_kv_heads, S, L.Sp, dh, P,
+                          kv->capacity ? kv->capacity : P, s);
+      if (l == c.n_layers - 1) break;  // nothing after the last layer's keys and values is needed
+    }
     AttnArgs aa;
     aa.q = qo.q;
     aa.k = qo.k;
@@ -259,6 +268,7 @@ int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_k
     aa.S = S;
     aa.Sp = L.Sp;
     aa.P = P;
+    aa.Pc = kv ? (kv->capacity ? kv->capacity : P) : 0;
     aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
     {
       PROF(P_ATTN);
@@ -597,6 +607,22 @@ dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S
   if (ev) (void)hipEventDestroy(ev);
   if (gs) (void)hipStreamDestroy(gs);
   return st;
+}
+
+dcl_status dcl_kv_append(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  if (!kv) return fail(DCL_E_ARG, "kv is NULL");
+  dcl_status st = check_step_args(m, tokens, B, S, kv, ws, ws_bytes);
+  if (st != DCL_OK) return st;
+  for (int l = 0; l < m->cfg.n_layers; ++l)
+    if (!kv->k[l] || !kv->v[l]) return fail(DCL_E_ARG, "kv cache pointer of layer %d is NULL", l);
+  const int cap = kv->capacity ? kv->capacity : kv->prefix_len;
+  if ((long)kv->prefix_len + S > cap)
+    return fail(DCL_E_ARG, "prefix_len %d + S %d exceeds the cache capacity %d", kv->prefix_len, S, cap);
+  (void)hipGetLastError();
+  run_forward(m, tokens, B, S, kv, ws, step_layout(m->cfg, B, S), stream, true);
+  return hip_check(hipGetLastError(), "kv_append launch");
 }
 
 struct ScoreLayout {

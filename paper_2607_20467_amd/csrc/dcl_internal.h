@@ -119,11 +119,15 @@ void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, floa
 // Non-causal attention over [cache (P keys) || fresh (S keys)].
 struct AttnArgs {
   const bf16_t *q, *k, *vt;      // [B,H,S,dh], [B,Hkv,S,dh], [B,Hkv,dh,Sp]
-  const bf16_t *kc, *vc;         // [B,Hkv,P,dh], [B,Hkv,dh,P] or null
+  const bf16_t *kc, *vc;         // [B,Hkv,Pc,dh], [B,Hkv,dh,Pc] (first P positions used) or null
   bf16_t* o;                     // [B,S,H*dh]
-  int B, H, Hkv, dh, S, Sp, P;
+  int B, H, Hkv, dh, S, Sp, P, Pc;
   float scale_log2;              // log2(e) / sqrt(dh)
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
+// Fresh keys k [B,Hkv,S,dh] and values vt [B,Hkv,dh,Sp] into a cache at positions [P, P + S)
+// (kc [B,Hkv,Pc,dh], vc [B,Hkv,dh,Pc]).
+void launch_kv_writeback(const bf16_t* k, const bf16_t* vt, bf16_t* kc, bf16_t* vc, int B, int Hkv, int S, int Sp,
+                         int dh, int P, int Pc, hipStream_t s);
 
 }  // namespace dcl

@@ -84,9 +84,9 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
     }
   }
   const size_t kvh = (size_t)b * a.Hkv + g;
-  const bf16_t* kc = a.kc ? a.kc + kvh * P * DH : nullptr;
+  const bf16_t* kc = a.kc ? a.kc + kvh * a.Pc * DH : nullptr;
   const bf16_t* kf = a.k + kvh * S * DH;
-  const bf16_t* vc = a.vc ? a.vc + kvh * DH * P : nullptr;
+  const bf16_t* vc = a.vc ? a.vc + kvh * DH * a.Pc : nullptr;
   const bf16_t* vf = a.vt + kvh * DH * a.Sp;
 
   auto issue = [&](int t) {
@@ -108,7 +108,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
         const int d = p2 >> 3, slot = p2 & 7;
         const int c = slot ^ (d & 7);
         const int j = k0 + c * 8;
-        if (j < P) src = vc + (size_t)d * P + j;
+        if (j < P) src = vc + (size_t)d * a.Pc + j;
         else if (j < nkeys) src = vf + (size_t)d * a.Sp + (j - P);
       }
       dma16(src, stage + q * 64);
@@ -248,5 +248,35 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.S >= 512) run_attn<8, 2>(a, s);
   else run_attn<4, 2>(a, s);
 }
+
+// ---------------------------------------------------------------- cache write-back
+// One thread per 16-byte key chunk, then one per value element (the value rows are key-contiguous
+// and the write offset P + s need not be 8-aligned at a ragged S).
+__global__ void __launch_bounds__(256) kv_writeback_kernel(const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
+                                                          bf16_t* __restrict__ kc, bf16_t* __restrict__ vc, int BH,
+                                                          int S, int Sp, int dh, int P, int Pc) {
+  const size_t nk = (size_t)BH * S * (dh / 8), nv = (size_t)BH * dh * S;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nk + nv; i += (size_t)gridDim.x * blockDim.x) {
+    if (i < nk) {
+      const size_t c = i % (dh / 8), rest = i / (dh / 8);
+      const size_t s = rest % S, bh = rest / S;
+      *reinterpret_cast<uint4*>(kc + (bh * Pc + P + s) * dh + 8 * c) =
+          *reinterpret_cast<const uint4*>(k + (bh * S + s) * dh + 8 * c);
+    } else {
+      const size_t e = i - nk;
+      const size_t s = e % S, rest = e / S;  // rest = bh * dh + d
+      vc[rest * Pc + P + s] = vt[rest * Sp + s];
+    }
+  }
+}
+
+void launch_kv_writeback(const bf16_t* k, const bf16_t* vt, bf16_t* kc, bf16_t* vc, int B, int Hkv, int S, int Sp,
+                         int dh, int P, int Pc, hipStream_t s) {
+  const size_t n = (size_t)B * Hkv * S * (dh / 8 + dh);
+  if (n == 0) return;
+  const int grid = (int)((n + 255) / 256 < 8 * 1024 ? (n + 255) / 256 : 8 * 1024);
+  hipLaunchKernelGGL(kv_writeback_kernel, dim3(grid), dim3(256), 0, s, k, vt, kc, vc, B * Hkv, S, Sp, dh, P, Pc);
+}
+
 
 }  // namespace dcl
