@@ -132,9 +132,13 @@ def pmc_summary(csv_path, copy_mib):
 
 
 def gpu_clock_mhz():
-    """Current shader clock reported by rocm-smi right after the timed steps (None if unavailable)."""
+    """Current shader clock reported by rocm-smi right after the timed steps (None if unavailable).
+    Not read under rocprofv3: its preloaded tool would initialise the GPU inside the rocm-smi child,
+    which then replaces itself with the Python interpreter."""
     import re
     import subprocess
+    if any(k.startswith("ROCPROF") for k in os.environ):
+        return None
     try:
         out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20).stdout
     except Exception:
