@@ -1,9 +1,9 @@
 // Non-causal (bidirectional) flash-style attention for gfx950, MHA and GQA, head_dim 64 / 128.
 //
 // Masked diffusion LMs attend from every position to every position; there is no causal mask, so
-// the whole S x S score matrix is real work. One workgroup handles 16*NW queries of one (batch,
-// head); each wavefront owns 16 queries and walks the keys in tiles of 64 with an online softmax
-// in float32. Keys are [cached prefix (P) || the S fresh tokens].
+// the whole S x S score matrix is real work. One workgroup handles 16*NQ queries of one (batch,
+// head); each wavefront owns 16 queries and walks its share of the keys in tiles of KT (32 or 64)
+// with an online softmax in float32. Keys are [cached prefix (P) || the S fresh tokens].
 //
 // Orientation: the score tile is computed transposed, S^T = K Q^T (MFMA A = K from LDS, B = Q held
 // in registers), so each lane holds 16 scores of ONE query. Its softmax probabilities then feed the
@@ -15,7 +15,6 @@
 
 namespace dcl {
 
-constexpr int KT = 64;  // keys per tile
 
 __device__ __attribute__((aligned(64))) uint4 g_attn_zero[4];
 
@@ -43,20 +42,48 @@ template <int N>
 __device__ __forceinline__ void attn_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
+// Wait until all but this wave's `newer` most recently issued stages (IPW loads each) landed.
+template <int IPW, int MAXN>
+__device__ __forceinline__ void attn_wait_stages(int newer) {
+  if constexpr (MAXN > 0) {
+    static_assert(MAXN * IPW < 64, "vmcnt range");
+    if (newer >= MAXN) {
+      attn_wait_vmcnt<MAXN * IPW>();
+      return;
+    }
+    attn_wait_stages<IPW, MAXN - 1>(newer);
+  } else {
+    attn_wait_vmcnt<0>();
+  }
+}
 
 // K and V^T tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 into a STAGES-deep ring (no
 // register staging, no padding). K rows (DH/8 chunks of 16 bytes) are XOR-swizzled by the key
-// index, V^T rows (8 chunks = 64 keys) by the dimension index, so the fragment reads below are
+// index, V^T rows (KT/8 chunks of 8 keys) by the dimension index, so the fragment reads below are
 // bank-conflict free. Chunks past the last key read a zero chunk.
-template <int NW, int DH, int STAGES>
-__global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
-  constexpr int BQ = 16 * NW, NT = NW * 64;
+//
+// Key groups: the NQ * KG waves of a workgroup are NQ query waves (16 queries each) times KG key
+// groups. Step t of the ring holds the KG key tiles t*KG .. t*KG + KG - 1; key group g works on
+// tile t*KG + g, so each wave's serial chain (scores -> softmax -> P V) covers 1/KG of the keys
+// and KG times as many waves hide each other's latencies. At the end the groups' running
+// (max, sum, unnormalised output) are combined through LDS in group order, which keeps the result
+// independent of timing.
+template <int NQ, int KG, int KT, int DH, int STAGES>
+__global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
+  constexpr int BQ = 16 * NQ, NWAVE = NQ * KG;
   constexpr int KC = DH / 8;           // chunks per K row
-  constexpr int KCH = KT * KC;         // K chunks per stage
-  constexpr int VCH = DH * (KT / 8);   // V^T chunks per stage
-  constexpr int SCH = KCH + VCH;       // chunks per stage
-  constexpr int IPW = SCH / 64 / NW;   // load instructions per wave per stage
-  static_assert(SCH % (64 * NW) == 0 && KCH % 64 == 0, "stage shape");
+  constexpr int VC = KT / 8;           // chunks per V^T row
+  constexpr int KCH = KT * KC;         // K chunks per tile
+  constexpr int VCH = DH * VC;         // V^T chunks per tile
+  constexpr int TCH = KCH + VCH;       // chunks per tile
+  constexpr int SCH = KG * TCH;        // chunks per ring step
+  constexpr int IPW = SCH / 64 / NWAVE;  // load instructions per wave per ring step
+  static_assert((KT == 32 || KT == 64) && SCH % (64 * NWAVE) == 0 && KCH % 64 == 0 && VCH % 64 == 0 &&
+                    STAGES >= 2 && IPW * (STAGES - 2) < 64 && NWAVE <= 16,
+                "stage shape");
+  static_assert(KG == 1 || (size_t)(KG - 1) * NQ * (DH / 16) * 64 * 16 + (size_t)(KG - 1) * NQ * 64 * 8 <=
+                                (size_t)STAGES * SCH * 16,
+                "the group merge reuses the ring");
   extern __shared__ __attribute__((aligned(1024))) uint4 sm[];
 
   // Units (batch, head, query tile), query tile innermost: XCD x (= blockIdx % 8) takes a contiguous
@@ -69,10 +96,12 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   const int qt = L % nqt, h = (L / nqt) % a.H, b = L / (nqt * a.H);
   const int g = h / (a.H / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int qw = wid % NQ, kg = wid / NQ;
   const int lq = lane & 15, lg = lane >> 4;
   const int S = a.S, P = a.P, nkeys = P + S;
-  const int qrow = qt * BQ + wid * 16 + lq;
+  const int qrow = qt * BQ + qw * 16 + lq;
   const int ntiles = (nkeys + KT - 1) / KT;
+  const int nsteps = (ntiles + KG - 1) / KG;
 
   bf16x8_t qf[DH / 32];
   {
@@ -89,95 +118,143 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   const bf16_t* vc = a.vc ? a.vc + kvh * DH * a.Pc : nullptr;
   const bf16_t* vf = a.vt + kvh * DH * a.Sp;
 
+  // Loop-invariant part of every DMA source: instruction i of this wave fills chunks
+  // [(wid*IPW + i)*64, +64) of a ring step, all inside one key group's K half or V^T half. Per
+  // ring step only the tile origin k0 changes: a chunk at key j < P comes from the cache, j < P + S
+  // from the fresh keys/values, beyond that from a zero chunk.
+  int jrel[IPW], offc[IPW], offf[IPW], sgrp[IPW];
+  bool isk[IPW];
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int q = wid * IPW + i;
+    sgrp[i] = (q * 64) / TCH;
+    const int pos = q * 64 + lane - sgrp[i] * TCH;
+    isk[i] = pos < KCH;
+    if (isk[i]) {  // K chunk: slot pos -> key row, chunk column
+      const int key = pos / KC, c = (pos % KC) ^ (key & (KC - 1));
+      jrel[i] = key;
+      offc[i] = key * DH + c * 8;
+      offf[i] = offc[i];
+    } else {       // V^T chunk: slot -> dimension row, 8-key chunk
+      const int p2 = pos - KCH;
+      const int d = p2 / VC, c = (p2 % VC) ^ (d & (VC - 1));
+      jrel[i] = c * 8;
+      offc[i] = d * a.Pc + c * 8;
+      offf[i] = d * a.Sp + c * 8;
+    }
+  }
   auto issue = [&](int t) {
     uint4* stage = sm + (t % STAGES) * SCH;
-    const int k0 = t * KT;
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
-      const int q = wid * IPW + i;
-      const int pos = q * 64 + lane;
-      const void* src = g_attn_zero;
-      if (q * 64 < KCH) {  // K chunk: slot pos -> key row, chunk column
-        const int key = pos / KC, slot = pos % KC;
-        const int c = slot ^ (key & (KC - 1));
-        const int j = k0 + key;
-        if (j < P) src = kc + (size_t)j * DH + c * 8;
-        else if (j < nkeys) src = kf + (size_t)(j - P) * DH + c * 8;
-      } else {             // V^T chunk: slot -> dimension row, 8-key chunk
-        const int p2 = pos - KCH;
-        const int d = p2 >> 3, slot = p2 & 7;
-        const int c = slot ^ (d & 7);
-        const int j = k0 + c * 8;
-        if (j < P) src = vc + (size_t)d * a.Pc + j;
-        else if (j < nkeys) src = vf + (size_t)d * a.Sp + (j - P);
-      }
-      dma16(src, stage + q * 64);
+      const int k0 = (t * KG + sgrp[i]) * KT;
+      const int j = k0 + jrel[i];
+      const int mult = isk[i] ? DH : 1;
+      const bf16_t* cb = isk[i] ? kc : vc;
+      const bf16_t* fb = isk[i] ? kf : vf;
+      const void* src = j < P ? static_cast<const void*>(cb + offc[i] + (size_t)k0 * mult)
+                      : j < nkeys ? static_cast<const void*>(fb + offf[i] + (ptrdiff_t)(k0 - P) * mult)
+                                  : static_cast<const void*>(g_attn_zero);
+      dma16(src, stage + (wid * IPW + i) * 64);
     }
   };
 
   f32x4_t o[DH / 16];
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m = -INFINITY, l = 0.f;
+  float m = -INFINITY, l = 0.f;  // running max (log2 units, scaled) and sum of this wave's queries
+  const float scale = a.scale_log2;
 
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
-    if (st < ntiles) issue(st);
-  for (int t = 0; t < ntiles; ++t) {
-    const int pending = min(STAGES - 2, ntiles - 1 - t);
-    if (STAGES >= 3 && pending >= 1) attn_wait_vmcnt<(STAGES >= 3 ? IPW : 0)>();
-    else attn_wait_vmcnt<0>();
+    if (st < nsteps) issue(st);
+  for (int t = 0; t < nsteps; ++t) {
+    // step t landed; the steps t + 1 .. min(nsteps - 1, t + STAGES - 2) may still fly
+    attn_wait_stages<IPW, STAGES - 2>(min(STAGES - 2, nsteps - 1 - t));
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (t + STAGES - 1 < ntiles) issue(t + STAGES - 1);
-    const uint4* sK = sm + (t % STAGES) * SCH;
+    if (t + STAGES - 1 < nsteps) issue(t + STAGES - 1);
+    const int k0 = (t * KG + kg) * KT;
+    if (k0 >= nkeys) continue;  // this group's tile is past the end (uniform per wave)
+    const uint4* sK = sm + (t % STAGES) * SCH + kg * TCH;
     const uint4* sV = sK + KCH;
-    const int k0 = t * KT;
 
-    // S^T = K Q^T: lane holds keys 16 kt + 4 lg + r of query lq
-    f32x4_t sc[KT / 16];
+    // S^T = K Q^T: lane holds keys 16 kt + 4 lg + r of query lq. The tile's K fragments are read
+    // first and the independent accumulation chains interleaved.
+    bf16x8_t kfr[KT / 16][DH / 32];
 #pragma unroll
     for (int kt = 0; kt < KT / 16; ++kt) {
-      sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       const int row = 16 * kt + lq;
 #pragma unroll
       for (int ks = 0; ks < DH / 32; ++ks) {
         const int c = 4 * ks + lg;
-        sc[kt] = mfma16a(__builtin_bit_cast(bf16x8_t, sK[row * KC + (c ^ (row & (KC - 1)))]), qf[ks], sc[kt]);
+        kfr[kt][ks] = __builtin_bit_cast(bf16x8_t, sK[row * KC + (c ^ (row & (KC - 1)))]);
       }
     }
+    f32x4_t sc[KT / 16];
+#pragma unroll
+    for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < DH / 32; ++ks)
+#pragma unroll
+      for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = mfma16a(kfr[kt][ks], qf[ks], sc[kt]);
+    // V^T fragments, read while the softmax below runs: dimension 16 dt + lq at the keys
+    // 32 s2 + 4 lg + {0..3} and 32 s2 + 16 + 4 lg + {0..3} (the order in which the score MFMA left
+    // the probabilities in the lanes)
+    bf16x8_t vfr[KT / 32][DH / 16];
+#pragma unroll
+    for (int s2 = 0; s2 < KT / 32; ++s2) {
+      const int c0 = 4 * s2 + (lg >> 1), c1 = c0 + 2, half = lg & 1;
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) {
+        const int d = 16 * dt + lq;
+        const uint2 v0 = reinterpret_cast<const uint2*>(sV + d * VC + (c0 ^ (d & (VC - 1))))[half];
+        const uint2 v1 = reinterpret_cast<const uint2*>(sV + d * VC + (c1 ^ (d & (VC - 1))))[half];
+        vfr[s2][dt] = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+      }
+    }
+    if (k0 + KT > nkeys) {  // only the last tile holds keys past the end
+#pragma unroll
+      for (int kt = 0; kt < KT / 16; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (k0 + 16 * kt + 4 * lg + r >= nkeys) sc[kt][r] = -INFINITY;
+    }
     float tmax = -INFINITY;
-    const bool tail = k0 + KT > nkeys;  // only the last tile holds keys past the end
 #pragma unroll
     for (int kt = 0; kt < KT / 16; ++kt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + 16 * kt + 4 * lg + r;
-        const float v = (!tail || key < nkeys) ? sc[kt][r] * a.scale_log2 : -INFINITY;
-        sc[kt][r] = v;
-        tmax = fmaxf(tmax, v);
-      }
+      for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, sc[kt][r]);
     // the four lane groups holding one query's keys: lanes l, l^16, l^32, l^48
     tmax = xor_lanes16(tmax, [](float x, float y) { return fmaxf(x, y); });
     tmax = xor_lanes32(tmax, [](float x, float y) { return fmaxf(x, y); });
-    const float mn = fmaxf(m, tmax);  // finite: every tile holds at least one key
-    const float alpha = __builtin_amdgcn_exp2f(m - mn);
+    // Lazy rescaling: the reference point m only moves when a score exceeds it by more than
+    // 2^8 (probabilities up to 256 are exact to represent and sum in float32); the division by
+    // the running sum at the end makes the result independent of the reference point. When no
+    // lane of the wave moves, the output rescale is skipped.
+    const float ts = tmax * scale;
+    const bool move = ts > m + 8.f;  // true on the first processed tile (m = -inf)
+    const float mn = move ? ts : m;
     float psum = 0.f;
 #pragma unroll
     for (int kt = 0; kt < KT / 16; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float pv = __builtin_amdgcn_exp2f(sc[kt][r] - mn);
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], scale, -mn));
         sc[kt][r] = pv;
         psum += pv;
       }
     psum = xor_lanes16(psum, [](float x, float y) { return x + y; });
     psum = xor_lanes32(psum, [](float x, float y) { return x + y; });
-    l = l * alpha + psum;
-    m = mn;
+    if (__builtin_amdgcn_ballot_w64(move)) {
+      const float alpha = __builtin_amdgcn_exp2f(m - mn);  // 1 in the lanes that keep m
+      l *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) o[dt] *= alpha;
+      for (int dt = 0; dt < DH / 16; ++dt) o[dt] *= alpha;
+    }
+    l += psum;
+    m = mn;
 
-    // O^T += V^T P^T over two 32-key steps; slot order: keys 32 s2 + 4 lg + {0..3}, then +16
+    // O^T += V^T P^T over 32-key steps; P enters as bf16 hi + lo parts
 #pragma unroll
     for (int s2 = 0; s2 < KT / 32; ++s2) {
       uint32_t hi[4], lo[4];
@@ -189,17 +266,37 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
       }
       const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
       const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-      const int c0 = 4 * s2 + (lg >> 1), c1 = c0 + 2, half = lg & 1;
 #pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) {
-        const int d = 16 * dt + lq;
-        const uint2* r0 = reinterpret_cast<const uint2*>(sV + d * 8 + (c0 ^ (d & 7))) + half;
-        const uint2* r1 = reinterpret_cast<const uint2*>(sV + d * 8 + (c1 ^ (d & 7))) + half;
-        const uint2 v0 = *r0, v1 = *r1;
-        const bf16x8_t va = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
-        o[dt] = mfma16a(va, phi, o[dt]);
-        o[dt] = mfma16a(va, plo, o[dt]);
-      }
+      for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], phi, o[dt]);
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], plo, o[dt]);
+    }
+  }
+
+  if constexpr (KG > 1) {
+    // groups 1 .. KG-1 park (m, l, o) in the ring; group 0 folds them in group order
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    f32x4_t* xo = reinterpret_cast<f32x4_t*>(sm);
+    float2* xml = reinterpret_cast<float2*>(xo + (size_t)(KG - 1) * NQ * (DH / 16) * 64);
+    if (kg > 0) {
+      const int base = (kg - 1) * NQ + qw;
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) xo[((size_t)base * (DH / 16) + dt) * 64 + lane] = o[dt];
+      xml[base * 64 + lane] = make_float2(m, l);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (kg > 0) return;
+#pragma unroll
+    for (int gg = 1; gg < KG; ++gg) {
+      const int base = (gg - 1) * NQ + qw;
+      const float2 ml = xml[base * 64 + lane];
+      if (ml.x == -INFINITY) continue;  // a group that saw no key
+      const float mn = fmaxf(m, ml.x);
+      const float ea = __builtin_amdgcn_exp2f(m - mn), eb = __builtin_amdgcn_exp2f(ml.x - mn);
+      l = l * ea + ml.y * eb;
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) o[dt] = o[dt] * ea + xo[((size_t)base * (DH / 16) + dt) * 64 + lane] * eb;
+      m = mn;
     }
   }
 
@@ -216,37 +313,42 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnArgs a) {
   }
 }
 
-template <int NW, int STAGES>
+template <int NQ, int KG, int KT, int STAGES>
 static void run_attn(const AttnArgs& a, hipStream_t s) {
-  const int units = ((a.S + 16 * NW - 1) / (16 * NW)) * a.H * a.B;
+  static_assert((size_t)STAGES * KG * (KT * 16 + 128 * (KT / 8)) * 16 <= 160 * 1024, "ring exceeds the LDS of a CU");
+  const int units = ((a.S + 16 * NQ - 1) / (16 * NQ)) * a.H * a.B;
+  if (units == 0) return;
   dim3 grid(8 * ((units + 7) / 8));
-  const size_t lds = (size_t)STAGES * (KT * (a.dh / 8) + a.dh * (KT / 8)) * 16;
+  const size_t lds = (size_t)STAGES * KG * (KT * (a.dh / 8) + a.dh * (KT / 8)) * 16;
   if (a.dh == 128) {
-    auto kern = attn_kernel<NW, 128, STAGES>;
+    auto kern = attn_kernel<NQ, KG, KT, 128, STAGES>;
     static bool set = false;
     if (!set) {
       (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       set = true;
     }
-    hipLaunchKernelGGL(kern, grid, dim3(NW * 64), lds, s, a);
+    hipLaunchKernelGGL(kern, grid, dim3(NQ * KG * 64), lds, s, a);
   } else {
-    auto kern = attn_kernel<NW, 64, STAGES>;
+    auto kern = attn_kernel<NQ, KG, KT, 64, STAGES>;
     static bool set = false;
     if (!set) {
       (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       set = true;
     }
-    hipLaunchKernelGGL(kern, grid, dim3(NW * 64), lds, s, a);
+    hipLaunchKernelGGL(kern, grid, dim3(NQ * KG * 64), lds, s, a);
   }
 }
 
-// A two-stage ring; 64 queries (4 waves) per workgroup for short blocks, 128 (8 waves) from 512
-// queries up, where eight waves share each key/value tile: measured on MI355X, 8 waves take 91 us
-// instead of 112 us for Dream-7B at 4 x 768 tokens and 95 instead of 104 us for LLaDA-8B at 1280,
-// while 4 waves stay best at 384 tokens and for 64-token blocks over a cached prefix.
+// A two-stage ring of 64-key tiles. Few query waves (B * H * S / 16 below 4096): 4 query waves
+// x 2 key groups per workgroup, so each wave walks half the keys and twice as many waves share a
+// CU; many query waves: 8 query waves x 1 group, whose 64 KB ring lets two workgroups share a CU.
+// Measured on MI355X (LLaDA-8B / Dream-7B heads): 384 tokens 13.0 us (18.2 with one group of 4),
+// 1280 tokens 90 us (98 with one group of 8), 8 x 64 tokens over a 1216-key cache 33 us (49 with
+// one group of 4), Dream-7B 4 x 768 tokens 95 us (119 with two groups of 4).
 void launch_attention(const AttnArgs& a, hipStream_t s) {
-  if (a.S >= 512) run_attn<8, 2>(a, s);
-  else run_attn<4, 2>(a, s);
+  const long query_waves = (long)a.B * a.H * ((a.S + 15) / 16);
+  if (query_waves >= 4096) run_attn<8, 1, 64, 2>(a, s);
+  else run_attn<4, 2, 64, 2>(a, s);
 }
 
 // ---------------------------------------------------------------- cache write-back

@@ -34,6 +34,16 @@ CASES = {
     "ragged": _variant("ragged", _W["c1s"],
                        dict(n_heads=2, n_kv_heads=1, head_dim=64, d_model=208, d_ffn=400, vocab=1000, mask_id=999),
                        batch=2, prompt_len=29, gen_len=48, window=16, p=29, draft=(45, 61)),
+    # 48 tokens: a single 64-key tile, so the second key group of the attention has no keys (on the
+    # well-conditioned tiny model: the spread one turns rare bf16 rounding flips into lse changes
+    # several times its float32 drift at this length, with either attention path)
+    "short": _variant("short", _W["c1"], {}, batch=2, prompt_len=16, gen_len=32, window=16, p=16, draft=(24, 40)),
+    # 16 x 16 heads x 256 tokens = 4096 query waves: the attention path with one key group of
+    # 8 query waves (head_dim 64, GQA 16/4, H*dh != d)
+    "many_heads": _variant("many_heads", _W["c1s"],
+                           dict(n_layers=1, n_heads=16, n_kv_heads=4, head_dim=64, d_model=512, d_ffn=512,
+                                vocab=1000, mask_id=999),
+                           batch=16, prompt_len=64, gen_len=192, window=32, p=64, draft=(128, 192)),
     # larger tile counts: S=320 (5 query tiles), vocab 8192, 3 layers
     "wide": _variant("wide", _W["c1s"], dict(n_layers=3, d_model=512, n_heads=8, n_kv_heads=8, d_ffn=1376,
                                              vocab=8192, mask_id=8191, weight_dtype="bf16"),
