@@ -34,13 +34,13 @@ int main(int argc, char** argv) {
   };
   size_t maxw = 0, maxx = 0, maxo = 0;
   for (auto& s : shapes) { maxw = std::max(maxw, (size_t)s.N * s.K); maxx = std::max(maxx, (size_t)s.T * s.K); maxo = std::max(maxo, (size_t)s.N * s.T); }
-  bf16_t *W, *X, *q, *k, *vt, *a; float *r, *P, *pm1, *pm2, *ps; int32_t *pi1, *pi2, *cnt; float2* rope;
+  bf16_t *W, *X, *q, *k, *vt, *a; float *r, *P, *pm1, *pm2, *ps, *pt; int32_t *pi1, *pi2, *cnt; float2* rope;
   const size_t pool = std::max(maxw, (size_t)1536 << 20);  // elements: 3 GiB of weights, far beyond the 256 MB MALL
   CK(hipMalloc(&W, pool * 2)); CK(hipMalloc(&X, maxx * 2));
   CK(hipMalloc(&q, maxo * 2)); CK(hipMalloc(&k, maxo * 2)); CK(hipMalloc(&vt, maxo * 2 + (1 << 20))); CK(hipMalloc(&a, maxo * 2));
   CK(hipMalloc(&r, maxo * 4)); CK(hipMalloc(&P, maxo * 4 * 4));
   const size_t lmp = (size_t)3072 * (152064 / 128 + 1);
-  CK(hipMalloc(&pm1, lmp * 4)); CK(hipMalloc(&pm2, lmp * 4)); CK(hipMalloc(&ps, lmp * 4));
+  CK(hipMalloc(&pm1, lmp * 4)); CK(hipMalloc(&pm2, lmp * 4)); CK(hipMalloc(&ps, lmp * 4)); CK(hipMalloc(&pt, lmp * 4));
   CK(hipMalloc(&pi1, lmp * 4)); CK(hipMalloc(&pi2, lmp * 4)); CK(hipMalloc(&cnt, 4));
   CK(hipMalloc(&rope, (size_t)4096 * 64 * 8)); CK(hipMemset(rope, 0, (size_t)4096 * 64 * 8));
   hipLaunchKernelGGL(fill, dim3((pool + 255) / 256), dim3(256), 0, 0, W, pool, 1u);
@@ -71,15 +71,15 @@ int main(int argc, char** argv) {
           const bf16_t* Wr = W + (size_t)(rot++ % ncopy) * wsz;
           if (s.kind == 'q') {
             QkvOut o{q, k, vt, nullptr, rope, s.H, s.Hkv, 128, S, (S + 7) / 8 * 8, 0};
-            run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiQkv{o}, 0);
+            run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiQkv{o}, 0);
           } else if (s.kind == 's') {
-            run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiSwiglu{a}, 0);
+            run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiSwiglu{a}, 0);
           } else if (s.kind == 'r') {
-            if (n > 1) run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiPartial{P, (size_t)s.T * s.N}, 0);
-            else run_plan(p, W, X, s.N, s.T, s.K, nullptr, EpiResid{r}, 0);
+            if (n > 1) run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiPartial{P, (size_t)s.T * s.N}, 0);
+            else run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiResid{r}, 0);
           } else {
-            LmOut o{pm1, pm2, ps, pi1, pi2, (s.N + kLmTile - 1) / kLmTile, cnt};
-            run_plan(p, W, X, s.N, s.T, s.K, cnt, EpiLm<128, 2>{o}, 0);
+            LmOut o{pm1, pm2, ps, pt, pi1, pi2, (s.N + kLmTile - 1) / kLmTile, cnt};
+            run_plan(p, Wr, X, s.N, s.T, s.K, cnt, EpiLm<128, 2>{o}, 0);
           }
         };
         for (int w = 0; w < 3; ++w) run();
