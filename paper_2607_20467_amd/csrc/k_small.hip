@@ -226,51 +226,77 @@ __device__ __forceinline__ Top2 top2_merge(Top2 a, Top2 b) {
   return o;
 }
 
-// One wavefront per scored row: fold the per-vocab-tile partials (m1, i1, m2, i2, s) in a fixed
-// order (lane-strided, then a fixed butterfly), so the result is bitwise reproducible.
-// conf = 1 / S, p2 = exp(m2 - M) / S, lse = M + log S with M = global max, S = sum_t s_t e^(m1_t - M).
+// Running (top-2, S, Tm) of a set of vocabulary tiles; S = sum exp(l - m1) and
+// Tm = sum exp(l - m1) (l - m1) are relative to the set's own top-1 value m1.
+struct RowAcc {
+  Top2 t;
+  float s, tm;
+};
+// Union of two disjoint sets: the relative sums move to the new top-1 value M (a term
+// exp(l - m) (l - m) becomes exp(l - M) (l - M) = e^(m-M) (exp(l - m) (l - m) + exp(l - m) (m - M))).
+// Symmetric in its arguments (distinct ids, commutative float adds), so every lane of a butterfly
+// computes the same bits.
+__device__ __forceinline__ RowAcc row_merge(const RowAcc& a, const RowAcc& b) {
+  RowAcc o;
+  o.t = top2_merge(a.t, b.t);
+  const float M = o.t.m1;
+  const bool ea_ok = a.t.m1 != -INFINITY, eb_ok = b.t.m1 != -INFINITY;
+  const float da = ea_ok ? a.t.m1 - M : 0.f, db = eb_ok ? b.t.m1 - M : 0.f;
+  const float ea = ea_ok ? __expf(da) : 0.f, eb = eb_ok ? __expf(db) : 0.f;
+  o.s = a.s * ea + b.s * eb;
+  o.tm = ea * (a.tm + a.s * da) + eb * (b.tm + b.s * db);
+  return o;
+}
+
+// One wavefront per scored row folds the row's per-vocabulary-tile partials in a fixed order:
+// lane l takes tiles l, l + 64, ... (four loads in flight per lane), then a fixed butterfly. The
+// result is bitwise reproducible. With M = the row maximum and S = sum_v exp(l_v - M):
+// conf = 1 / S, p2 = exp(m2 - M) / S, lse = M + log S, entropy = log S - Tm / S.
 __global__ void __launch_bounds__(256) merge_kernel(const float* __restrict__ pm1, const int32_t* __restrict__ pi1,
                                                    const float* __restrict__ pm2, const int32_t* __restrict__ pi2,
                                                    const float* __restrict__ ps, const float* __restrict__ pt,
                                                    int n_vt, const int32_t* __restrict__ rows,
                                                    const int32_t* __restrict__ count, dcl_row_stats st) {
-  int lane = threadIdx.x & 63;
-  int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (j >= *count) return;
   const size_t base = (size_t)j * n_vt;
-  Top2 t = {-INFINITY, -INFINITY, INT_MAX, INT_MAX};
-  for (int v = lane; v < n_vt; v += 64) {
-    Top2 x = {pm1[base + v], pm2[base + v], pi1[base + v], pi2[base + v]};
-    t = top2_merge(t, x);
+  RowAcc acc = {{-INFINITY, -INFINITY, INT_MAX, INT_MAX}, 0.f, 0.f};
+  constexpr int U = 4;
+  for (int v0 = lane; v0 < n_vt; v0 += 64 * U) {
+    RowAcc x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + 64 * u;
+      if (v < n_vt) {
+        x[u].t = {pm1[base + v], pm2[base + v], pi1[base + v], pi2[base + v]};
+        x[u].s = ps[base + v];
+        x[u].tm = pt[base + v];
+      } else {
+        x[u] = {{-INFINITY, -INFINITY, INT_MAX, INT_MAX}, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc = row_merge(acc, x[u]);
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
-    Top2 x = {__shfl_xor(t.m1, o, 64), __shfl_xor(t.m2, o, 64), __shfl_xor(t.i1, o, 64), __shfl_xor(t.i2, o, 64)};
-    t = top2_merge(t, x);  // symmetric (distinct ids), so every lane computes the same result
-  }
-  const float M = t.m1;
-  // S = sum_v exp(l_v - M), Tm = sum_v exp(l_v - M) (l_v - M) from the tiles' relative sums
-  float s = 0.f, tm = 0.f;
-  for (int v = lane; v < n_vt; v += 64) {
-    const float m = pm1[base + v];
-    if (m == -INFINITY) continue;  // a tile with no ids left
-    const float d = m - M, e = __expf(d), sv = ps[base + v];
-    s += sv * e;
-    tm += e * (pt[base + v] + sv * d);
-  }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    s += __shfl_xor(s, o, 64);
-    tm += __shfl_xor(tm, o, 64);
+    RowAcc x;
+    x.t = {__shfl_xor(acc.t.m1, o, 64), __shfl_xor(acc.t.m2, o, 64), __shfl_xor(acc.t.i1, o, 64),
+           __shfl_xor(acc.t.i2, o, 64)};
+    x.s = __shfl_xor(acc.s, o, 64);
+    x.tm = __shfl_xor(acc.tm, o, 64);
+    acc = row_merge(acc, x);
   }
   if (lane == 0) {
-    int row = rows[j];
-    st.top1[row] = t.i1;
-    st.top2[row] = t.i2;
+    const int row = rows[j];
+    const float s = acc.s;
+    st.top1[row] = acc.t.i1;
+    st.top2[row] = acc.t.i2;
     st.conf[row] = 1.0f / s;
-    st.p2[row] = __expf(t.m2 - M) / s;
-    st.lse[row] = M + logf(s);
-    if (st.entropy) st.entropy[row] = logf(s) - tm / s;  // H = log S - Tm / S
+    st.p2[row] = __expf(acc.t.m2 - acc.t.m1) / s;
+    st.lse[row] = acc.t.m1 + logf(s);
+    if (st.entropy) st.entropy[row] = logf(s) - acc.tm / s;
   }
 }
 
