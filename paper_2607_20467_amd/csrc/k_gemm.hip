@@ -213,19 +213,29 @@ __device__ __forceinline__ Part part_merge(const Part& a, const Part& b) {
   return o;
 }
 
-// LM head: one partial per (token, vocabulary tile of BW ids). Within a wave: per-lane scan of its
-// values, butterfly over the four lanes holding the same token, then a second pass for the sum of
-// exp(l - m1_wave). Waves that split the tile's vocabulary rows merge through LDS in wave order.
+// LM head: one partial per (token, vocabulary tile of kLmTile ids). Within a wave: per-lane scan of
+// its values, butterfly over the four lanes holding the same token, then a second pass for the sum
+// of exp(l - m1_wave). A wave whose weight rows span a whole vocabulary tile (16 * SW == kLmTile)
+// writes that tile's partial itself; otherwise the WW waves of a BW = kLmTile workgroup tile split
+// its vocabulary rows and merge through LDS in wave order.
 template <int BW, int WW>
 struct EpiLm {
   LmOut o;
   static constexpr bool kPartial = false;
+  // [wave along W][token within the workgroup tile] (BT <= 256); only the split-tile layout uses it
+  __device__ static Part (*xch_slot())[256] {
+    __shared__ Part xch[WW][256];
+    return xch;
+  }
   template <int SW, int ST>
   __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int tile_w, int) const {
-    __shared__ Part xch[WW][256];  // [wave along W][token within the workgroup tile]; BT <= 256
+    constexpr bool kOwn = 16 * SW == kLmTile;  // this wave covers a whole vocabulary tile
+    // any other layout is never planned for the LM head (plan_gemm's lm_ok); nothing to instantiate
+    if constexpr (!kOwn && !(BW == kLmTile && 16 * SW * WW == BW)) return;
     const int wid = threadIdx.x >> 6;
     const int wave_w = wid % WW, wave_t = wid / WW;
     const int R = *o.count;
+    const int vt = kOwn ? wb / kLmTile : tile_w;  // vocabulary tile of this wave's partial
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -266,18 +276,19 @@ struct EpiLm {
       t += __shfl_xor(t, 32, 64);
       p.s = s;
       p.t = t;
-      if (WW == 1) {
+      if constexpr (kOwn || WW == 1) {
         const int t = tl + 16 * j;
-        if (lane < 16 && t < R && t < T) {
-          const size_t idx = (size_t)t * o.n_vt + tile_w;
+        if (lane < 16 && t < R && t < T && vt < o.n_vt) {
+          const size_t idx = (size_t)t * o.n_vt + vt;
           o.pm1[idx] = p.m1; o.pi1[idx] = p.i1; o.pm2[idx] = p.m2; o.pi2[idx] = p.i2; o.ps[idx] = p.s;
           o.pt[idx] = p.t;
         }
-      } else if (lane < 16) {
-        xch[wave_w][(wave_t * ST + j) * 16 + lane] = p;
+      } else {
+        if (lane < 16) xch_slot()[wave_w][(wave_t * ST + j) * 16 + lane] = p;
       }
     }
-    if (WW > 1) {
+    if constexpr (!kOwn && WW > 1) {
+      Part(*xch)[256] = xch_slot();
       __syncthreads();
       if (wave_w == 0) {
 #pragma unroll
@@ -612,7 +623,8 @@ static const TileCfg kCfgs[] = {
     {160, 128, 128, 2, 2, 4, 0}, {96, 192, 128, 2, 2, 4, 0},  {192, 192, 64, 3, 4, 4, 0},
     {128, 128, 128, 2, 2, 4, 0}, {64, 192, 128, 2, 2, 4, 0},  {128, 192, 128, 2, 4, 4, 0},
     {128, 128, 64, 3, 2, 4, 0},  {128, 256, 64, 3, 2, 8, 0},  {128, 192, 64, 3, 2, 4, 0},
-    {128, 256, 64, 2, 2, 8, 0},
+    {128, 256, 64, 2, 2, 8, 0},  {256, 256, 64, 2, 2, 4, 0},  {256, 192, 64, 2, 2, 4, 0},
+    {256, 128, 64, 3, 2, 2, 0},
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kCUs = 256;
@@ -648,7 +660,9 @@ static double plan_cost(const TileCfg& c, int n, int Nw, int T, int K) {
 // force_bw != 0 (the LM head): the tile must be force_bw weight rows split over exactly
 // kLmWaves waves along W, the layout the top-2 epilogue's cross-wave merge is written for.
 static bool lm_ok(const TileCfg& c, int force_bw) {
-  return !force_bw || (c.bw == force_bw && c.ww == kLmWaves && cfg_lds(c) + kLmEpiLds <= kLdsBytes);
+  if (!force_bw || c.rp) return !force_bw;
+  if (c.bw / c.ww == force_bw) return cfg_lds(c) <= kLdsBytes;  // each wave owns a vocabulary tile
+  return c.bw == force_bw && c.ww == kLmWaves && cfg_lds(c) + kLmEpiLds <= kLdsBytes;
 }
 
 GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
@@ -733,7 +747,10 @@ static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw
     case 15: run_cfg<128, 128, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 16: run_cfg<128, 256, 64, 3, 2, 8>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 17: run_cfg<128, 192, 64, 3, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
-    default: run_cfg<128, 256, 64, 2, 2, 8>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 18: run_cfg<128, 256, 64, 2, 2, 8>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 19: run_cfg<256, 256, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 20: run_cfg<256, 192, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    default: run_cfg<256, 128, 64, 3, 2, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
   }
 }
 

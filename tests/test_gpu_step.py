@@ -44,6 +44,10 @@ CASES = {
                            dict(n_layers=1, n_heads=16, n_kv_heads=4, head_dim=64, d_model=512, d_ffn=512,
                                 vocab=1000, mask_id=999),
                            batch=16, prompt_len=64, gen_len=192, window=32, p=64, draft=(128, 192)),
+    # vocabulary 50001 at 192 rows: the LM head runs 256-id workgroup tiles whose two waves each own
+    # a 128-id vocabulary tile; 391 tiles, the last one 81 ids wide, the last workgroup's second
+    # wave past the end
+    "vocab_50001": _variant("vocab_50001", _W["c1"], dict(vocab=50001, mask_id=50000), batch=2),
     # larger tile counts: S=320 (5 query tiles), vocab 8192, 3 layers
     "wide": _variant("wide", _W["c1s"], dict(n_layers=3, d_model=512, n_heads=8, n_kv_heads=8, d_ffn=1376,
                                              vocab=8192, mask_id=8191, weight_dtype="bf16"),
@@ -77,7 +81,7 @@ def test_step_parity(key):
     compare_stats(stats_to_np(st), ref, w.tau_commit, w.tau_draft, what=key, conf_tol=ct, logit_tol=lt)
 
 
-@pytest.mark.parametrize("key", ["c1", "c1s", "ragged", "gqa_bias_dh128", "wide", "llada_2l"])
+@pytest.mark.parametrize("key", ["c1", "c1s", "ragged", "gqa_bias_dh128", "wide", "vocab_50001", "llada_2l"])
 def test_lm_head_on_gpu_hidden_exact_bar(key):
     """Exact-input stage: the GPU's float32 logits equal h_f W_lm^T (float64) of the GPU's own bf16 final
     hidden states within 2e-2, and those hidden states stay close to the oracle's."""
