@@ -30,11 +30,15 @@ __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint3
 // destination: the compiler then neither counts the copy as outstanding LDS traffic (which makes
 // it wait for lgkmcnt(0) before every fragment read) nor inserts vmcnt(0) before LDS reads that
 // might alias it. Callers track completion themselves (s_waitcnt vmcnt + barrier).
-__device__ __forceinline__ void dma16(const void* g, const void* lds) {
-  const uint32_t m0v =
-      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0v), "v"(g) : "memory", "m0");
+__device__ __forceinline__ void dma16_at(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               ::"s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(g) : "memory", "m0");
 }
+// LDS byte address of a pointer into __shared__ memory (wave-uniform, no null check)
+__device__ __forceinline__ uint32_t lds_addr_of(const void* lds) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
+}
+__device__ __forceinline__ void dma16(const void* g, const void* lds) { dma16_at(g, lds_addr_of(lds)); }
 
 // Packed-weight layout (byte offsets into the caller's weight buffer).
 struct LayerOffsets {

@@ -11,12 +11,13 @@
 // LDS tile in the matching key order; no register shuffle of P is needed.
 // P is split into bf16 hi + lo parts (two MFMAs), so the probabilities enter the product with
 // ~16 significant bits instead of 8.
+#include <type_traits>
+
 #include "dcl_internal.h"
 
 namespace dcl {
 
 
-__device__ __attribute__((aligned(64))) uint4 g_attn_zero[4];
 
 __device__ __forceinline__ f32x4_t mfma16a(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -95,7 +96,7 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   if (L >= units) return;
   const int qt = L % nqt, h = (L / nqt) % a.H, b = L / (nqt * a.H);
   const int g = h / (a.H / a.Hkv);
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qw = wid % NQ, kg = wid / NQ;
   const int lq = lane & 15, lg = lane >> 4;
   const int S = a.S, P = a.P, nkeys = P + S;
@@ -118,52 +119,69 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   const bf16_t* vc = a.vc ? a.vc + kvh * DH * a.Pc : nullptr;
   const bf16_t* vf = a.vt + kvh * DH * a.Sp;
 
-  // Loop-invariant part of every DMA source: instruction i of this wave fills chunks
-  // [(wid*IPW + i)*64, +64) of a ring step, all inside one key group's K half or V^T half. Per
-  // ring step only the tile origin k0 changes: a chunk at key j < P comes from the cache, j < P + S
-  // from the fresh keys/values, beyond that from a zero chunk.
-  int jrel[IPW], offc[IPW], offf[IPW], sgrp[IPW];
-  bool isk[IPW];
-#pragma unroll
-  for (int i = 0; i < IPW; ++i) {
-    const int q = wid * IPW + i;
-    sgrp[i] = (q * 64) / TCH;
-    const int pos = q * 64 + lane - sgrp[i] * TCH;
-    isk[i] = pos < KCH;
-    if (isk[i]) {  // K chunk: slot pos -> key row, chunk column
-      const int key = pos / KC, c = (pos % KC) ^ (key & (KC - 1));
-      jrel[i] = key;
-      offc[i] = key * DH + c * 8;
-      offf[i] = offc[i];
-    } else {       // V^T chunk: slot -> dimension row, 8-key chunk
-      const int p2 = pos - KCH;
-      const int d = p2 / VC, c = (p2 % VC) ^ (d & (VC - 1));
-      jrel[i] = c * 8;
-      offc[i] = d * a.Pc + c * 8;
-      offf[i] = d * a.Sp + c * 8;
-    }
-  }
-  auto issue = [&](int t) {
-    uint4* stage = sm + (t % STAGES) * SCH;
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int k0 = (t * KG + sgrp[i]) * KT;
-      const int j = k0 + jrel[i];
-      const int mult = isk[i] ? DH : 1;
-      const bf16_t* cb = isk[i] ? kc : vc;
-      const bf16_t* fb = isk[i] ? kf : vf;
-      const void* src = j < P ? static_cast<const void*>(cb + offc[i] + (size_t)k0 * mult)
-                      : j < nkeys ? static_cast<const void*>(fb + offf[i] + (ptrdiff_t)(k0 - P) * mult)
-                                  : static_cast<const void*>(g_attn_zero);
-      dma16(src, stage + (wid * IPW + i) * 64);
-    }
-  };
-
   f32x4_t o[DH / 16];
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;  // running max (log2 units, scaled) and sum of this wave's queries
   const float scale = a.scale_log2;
+
+  // DMA assignment: instruction i of wave w fills the 64-chunk block b = i * NWAVE + w of a ring
+  // step (block sizes are multiples of NWAVE, so the key group and the K / V^T role of instruction i
+  // are compile-time). Per ring step only the tile origin k0 changes: a chunk at key j < P comes
+  // from the cache, j < P + S from the fresh keys/values. A chunk past the last key re-reads the
+  // last key's (or last 8-key chunk's) data: those keys score -inf, so their probability is
+  // exactly 0 against finite values, and the address stays branch-free.
+  static_assert((KCH / 64) % NWAVE == 0 && (VCH / 64) % NWAVE == 0, "DMA blocks per wave");
+  constexpr int TB = TCH / 64;  // 64-chunk blocks per key tile
+  int jrel[IPW], offc[IPW];
+  const bf16_t* fsrc[IPW];  // fresh-key source for the tile origin k0 = P
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int bb = (i * NWAVE) % TB;       // block within the key tile (same for every wave's lane 0)
+    const int pos = (bb + wid) * 64 + lane;  // chunk within the key tile
+    if ((i * NWAVE) % TB < KCH / 64) {     // K chunk: slot pos -> key row, chunk column
+      const int key = pos / KC, c = (pos % KC) ^ (key & (KC - 1));
+      jrel[i] = key;
+      offc[i] = key * DH + c * 8;
+      fsrc[i] = kf + key * DH + c * 8;
+    } else {                                // V^T chunk: slot -> dimension row, 8-key chunk
+      const int p2 = pos - KCH;
+      const int d = p2 / VC, c = (p2 % VC) ^ (d & (VC - 1));
+      jrel[i] = c * 8;
+      offc[i] = d * a.Pc + c * 8;
+      fsrc[i] = vf + (size_t)d * a.Sp + c * 8;
+    }
+  }
+  const uint32_t lds_base = lds_addr_of(sm) + (uint32_t)wid * 1024u;
+  const int klast = nkeys - 1, vlast = (nkeys - 1) & ~7;  // last key, start of the last 8-key chunk
+  const int vlast_f = (S - 1) & ~7;                          // the same for the fresh values alone
+  // the main loop below is instantiated twice: without (kFresh) and with a cached prefix
+  auto main_loop = [&](auto fresh_only) {
+  constexpr bool kFresh = decltype(fresh_only)::value;
+  auto issue = [&](int t) {
+    const uint32_t stage = lds_base + (uint32_t)((t % STAGES) * SCH) * 16u;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const bool isk = (i * NWAVE) % TB < KCH / 64;
+      const int mult = isk ? DH : 1;
+      const int k0 = (t * KG + (i * NWAVE) / TB) * KT;
+      const int j = k0 + jrel[i];
+      const void* src;
+      if constexpr (kFresh) {
+        const int jc = min(j, isk ? klast : vlast);
+        src = fsrc[i] + (ptrdiff_t)(jc - jrel[i]) * mult;
+      } else {
+        // fresh side with the same clamping as above, in fresh-key indices; the cache side holds
+        // keys j < P (P is a multiple of 8, so no 8-key chunk straddles the two)
+        const int jf = min(j - P, isk ? klast - P : vlast_f);
+        const bf16_t* fp = fsrc[i] + (ptrdiff_t)(jf - jrel[i]) * mult;
+        const bf16_t* cp = (isk ? kc : vc) + offc[i] + (ptrdiff_t)k0 * mult;
+        src = j < P ? cp : fp;
+      }
+      dma16_at(src, stage + (uint32_t)(i * NWAVE) * 1024u);
+    }
+  };
+
 
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
@@ -272,6 +290,10 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
       for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], plo, o[dt]);
     }
   }
+
+  };
+  if (P == 0) main_loop(std::integral_constant<bool, true>{});
+  else main_loop(std::integral_constant<bool, false>{});
 
   if constexpr (KG > 1) {
     // groups 1 .. KG-1 park (m, l, o) in the ring; group 0 folds them in group order
