@@ -8,6 +8,8 @@
 #include <cstdio>
 #include <cstdlib>
 #include <vector>
+#include <algorithm>
+#include <utility>
 #include <string>
 using namespace dcl;
 #define CK(x) do { hipError_t e = (x); if (e != hipSuccess) { printf("HIP error %s at %d\n", hipGetErrorString(e), __LINE__); exit(1);} } while (0)
@@ -47,6 +49,10 @@ int main(int argc, char** argv) {
   hipLaunchKernelGGL(fill, dim3((maxx + 255) / 256), dim3(256), 0, 0, X, maxx, 2u);
   CK(hipDeviceSynchronize());
   hipEvent_t e0, e1; CK(hipEventCreate(&e0)); CK(hipEventCreate(&e1));
+  // bring the clocks to their loaded state before the first timing (about 0.3 s of GEMMs)
+  for (int w = 0; w < 200; ++w)
+    run_plan(GemmPlan{11, 1, 0}, W + (size_t)(w % 8) * 24576 * 4096, X, 24576, 384, 4096, nullptr, EpiSwiglu{a}, 0);
+  CK(hipDeviceSynchronize());
   for (size_t si = 0; si < shapes.size(); ++si) {
     if (only >= 0 && (int)si != only) continue;
     const Shape& s = shapes[si];
@@ -56,6 +62,40 @@ int main(int argc, char** argv) {
            plan_gemm(s.N, s.T, s.K, s.kind == 'l' ? kLmTile : 0, s.kind == 'r' ? kMaxSplit : 1).cfg,
            plan_gemm(s.N, s.T, s.K, s.kind == 'l' ? kLmTile : 0, s.kind == 'r' ? kMaxSplit : 1).nsplit);
     if (s.kind == 'l') { int R = s.R; CK(hipMemcpy(cnt, &R, 4, hipMemcpyHostToDevice)); }
+    // time plan p over `reps` calls (after 3 warm-up calls); weights rotate through the pool
+    auto measure = [&](const GemmPlan& p, int reps) {
+      const size_t wsz = (size_t)s.N * s.K;
+      const int ncopy = (int)std::max<size_t>(1, pool / wsz);
+      const int n = p.nsplit;
+      int rot = 0;
+      auto run = [&]() {
+        const bf16_t* Wr = W + (size_t)(rot++ % ncopy) * wsz;
+        if (s.kind == 'q') {
+          QkvOut o{q, k, vt, nullptr, rope, s.H, s.Hkv, 128, S, (S + 7) / 8 * 8, 0};
+          run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiQkv{o}, 0);
+        } else if (s.kind == 's') {
+          run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiSwiglu{a}, 0);
+        } else if (s.kind == 'r') {
+          if (n > 1) run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiPartial{P, (size_t)s.T * s.N}, 0);
+          else run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiResid{r}, 0);
+        } else {
+          LmOut o{pm1, pm2, ps, pt, pi1, pi2, (s.N + kLmTile - 1) / kLmTile, cnt};
+          run_plan(p, Wr, X, s.N, s.T, s.K, cnt, EpiLm<128, 2>{o}, 0);
+        }
+      };
+      for (int w = 0; w < 3; ++w) run();
+      CK(hipDeviceSynchronize());
+      CK(hipEventRecord(e0, 0));
+      for (int rr = 0; rr < reps; ++rr) run();
+      CK(hipEventRecord(e1, 0)); CK(hipEventSynchronize(e1));
+      float ms; CK(hipEventElapsedTime(&ms, e0, e1));
+      // split-K slices are added by the next RMSNorm: charge their extra traffic (~2 x 4 B per slice)
+      // at 12 TB/s, the rate the RMSNorm reads them while they are still cache-resident (at 384
+      // tokens it takes 8.8 us with four slices and 6.75 us with two)
+      const double pen = n > 1 ? (double)(n - 1) * s.T * s.N * 8 / 12.0e12 * 1e6 : 0.0;
+      return std::make_pair(1000.0 * ms / reps, pen);
+    };
+    std::vector<std::pair<double, GemmPlan>> all;
     for (int ci = 0; ci < kNumCfgs; ++ci) {
       const TileCfg& c = kCfgs[ci];
       if (s.kind == 'l' && !lm_ok(c, kLmTile)) continue;
@@ -63,40 +103,26 @@ int main(int argc, char** argv) {
       for (int n = 1; n <= maxn; ++n) {
         if (n > 1 && (s.K / 64) / n < 8) continue;
         if (n > 1 && c.rp) continue;
-        GemmPlan p{ci, n, 0};
-        const size_t wsz = (size_t)s.N * s.K;
-        const int ncopy = (int)std::max<size_t>(1, pool / wsz);
-        int rot = 0;
-        auto run = [&]() {
-          const bf16_t* Wr = W + (size_t)(rot++ % ncopy) * wsz;
-          if (s.kind == 'q') {
-            QkvOut o{q, k, vt, nullptr, rope, s.H, s.Hkv, 128, S, (S + 7) / 8 * 8, 0};
-            run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiQkv{o}, 0);
-          } else if (s.kind == 's') {
-            run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiSwiglu{a}, 0);
-          } else if (s.kind == 'r') {
-            if (n > 1) run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiPartial{P, (size_t)s.T * s.N}, 0);
-            else run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiResid{r}, 0);
-          } else {
-            LmOut o{pm1, pm2, ps, pt, pi1, pi2, (s.N + kLmTile - 1) / kLmTile, cnt};
-            run_plan(p, Wr, X, s.N, s.T, s.K, cnt, EpiLm<128, 2>{o}, 0);
-          }
-        };
-        for (int w = 0; w < 3; ++w) run();
-        CK(hipDeviceSynchronize());
-        const int reps = 20;
-        CK(hipEventRecord(e0, 0));
-        for (int rr = 0; rr < reps; ++rr) run();
-        CK(hipEventRecord(e1, 0)); CK(hipEventSynchronize(e1));
-        float ms; CK(hipEventElapsedTime(&ms, e0, e1));
-        const double us = 1000.0 * ms / reps;
-        // split-K slices are added by the next RMSNorm: charge their extra traffic (~2 x 4 B per slice)
-        const double pen = n > 1 ? (double)(n - 1) * s.T * s.N * 8 / 5.0e12 * 1e6 : 0.0;
+        const GemmPlan p{ci, n, 0};
+        const auto [us, pen] = measure(p, 20);
         printf("  cfg %2d (%3dx%3d k%3d s%d w%dx%d%s) split %d: %8.1f us (+%.1f slices)  %7.1f TFLOP/s\n", ci, c.bw, c.bt,
                c.kd, c.stages, c.ww, c.wt, c.rp ? " rp" : "", n, us, pen,
                2.0 * s.N * (s.kind == 'l' ? s.R : s.T) * s.K / us / 1e6);
-        if (us + pen < best) { best = us + pen; bc = ci; bn = n; }
+        all.push_back({us + pen, p});
       }
+    }
+    // the three fastest are timed again, interleaved, three times each; the lowest mean wins
+    std::sort(all.begin(), all.end(), [](const auto& x, const auto& y) { return x.first < y.first; });
+    const int top = (int)std::min<size_t>(3, all.size());
+    std::vector<double> sum(top, 0.0);
+    for (int round = 0; round < 3; ++round)
+      for (int c = 0; c < top; ++c) {
+        const auto [us, pen] = measure(all[c].second, 20);
+        sum[c] += us + pen;
+      }
+    for (int c = 0; c < top; ++c) {
+      printf("  again cfg %2d split %d: %8.1f us\n", all[c].second.cfg, all[c].second.nsplit, sum[c] / 3);
+      if (sum[c] / 3 < best) { best = sum[c] / 3; bc = all[c].second.cfg; bn = all[c].second.nsplit; }
     }
     printf("BEST {%d, %d, %d, %d, %d},  // %s: %.1f us\n", s.N, s.T, s.K, bc, bn, s.name.c_str(), best);
     fflush(stdout);

@@ -624,7 +624,7 @@ static const TileCfg kCfgs[] = {
     {128, 128, 128, 2, 2, 4, 0}, {64, 192, 128, 2, 2, 4, 0},  {128, 192, 128, 2, 4, 4, 0},
     {128, 128, 64, 3, 2, 4, 0},  {128, 256, 64, 3, 2, 8, 0},  {128, 192, 64, 3, 2, 4, 0},
     {128, 256, 64, 2, 2, 8, 0},  {256, 256, 64, 2, 2, 4, 0},  {256, 192, 64, 2, 2, 4, 0},
-    {256, 128, 64, 3, 2, 2, 0},
+    {256, 128, 64, 3, 2, 2, 0},  {256, 256, 64, 2, 4, 2, 0},
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kCUs = 256;
@@ -750,7 +750,8 @@ static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw
     case 18: run_cfg<128, 256, 64, 2, 2, 8>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 19: run_cfg<256, 256, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 20: run_cfg<256, 192, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
-    default: run_cfg<256, 128, 64, 3, 2, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 21: run_cfg<256, 128, 64, 3, 2, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    default: run_cfg<256, 256, 64, 2, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
   }
 }
 
