@@ -350,6 +350,8 @@ static void run_attn(const AttnArgs& a, hipStream_t s) {
       set = true;
     }
     hipLaunchKernelGGL(kern, grid, dim3(NQ * KG * 64), lds, s, a);
+  } else if constexpr ((KT * 8 / 64) % (NQ * KG) != 0 || (64 * (KT / 8) / 64) % (NQ * KG) != 0) {
+    run_attn<4, 2, 64, 2>(a, s);  // this wave layout does not tile head_dim 64: the default one does
   } else {
     auto kern = attn_kernel<NQ, KG, KT, 64, STAGES>;
     static bool set = false;
