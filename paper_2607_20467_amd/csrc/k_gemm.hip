@@ -9,12 +9,15 @@
 //          scattered to q [B,H,S,dh], k [B,Hkv,S,dh] and key-contiguous v [B,Hkv,dh,Sp];
 //   RESID  r[t, w] += C (float32 residual stream);
 //   SWIGLU a[t, f] = bf16(silu(gate) * up) (gate/up rows interleaved at load);
-//   LMHEAD per (token, 128-id vocabulary tile): top-1, top-2 and sum exp(l - top1) — logits stay
-//          in registers and never reach memory;
+//   LMHEAD per (token, 128-id vocabulary tile): top-1, top-2, sum exp(l - top1) and the entropy
+//          sum — logits stay in registers and never reach memory;
+//   PARTIAL float32 split-K slice, folded into the residual stream by the next RMSNorm;
 //   F32    plain float32 store (debug logits).
-// Tiles: BW weight rows x BT tokens per workgroup, K staged through LDS in steps of 64 with a
-// register prefetch of the next step and double-buffered LDS. The block -> tile map is XCD-aware:
-// consecutive tiles (which share a weight tile) land on the same XCD and its L2.
+// Tiles: BW weight rows x BT tokens per workgroup, K staged through a multi-stage LDS ring of
+// 64- or 128-deep slices filled by direct-to-LDS DMA (gemm_kernel), or through registers
+// (gemm_rp_kernel). The unit -> workgroup map is XCD-aware: consecutive tiles (which share a
+// weight tile) land on the same XCD and its L2. The configuration of each GEMM shape comes from a
+// measured table (gemm_tuned.inc), other shapes from a cost model.
 #include <float.h>
 #include <limits.h>
 
@@ -22,8 +25,6 @@
 
 namespace dcl {
 
-constexpr int BK = 64;        // K elements per LDS stage
-constexpr int LDSP = BK + 8;  // padded LDS row (144 bytes): conflict-free 16-byte fragment reads
 
 __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
