@@ -147,7 +147,8 @@ size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_p
  * memory. Token i is at absolute position kv_prefix + i; with kv == NULL the forward covers the
  * S tokens alone, otherwise they also attend to the cached prefix. Token ids outside
  * [0, vocab) read an all-zero embedding row. Writes `out` (all B*S rows). ws: device,
- * ws_bytes >= dcl_workspace_bytes(model, B, S, prefix), 256-byte aligned. */
+ * ws_bytes >= dcl_workspace_bytes(model, B, S, prefix), 256-byte aligned. Sizes: B*S <= 2^22 and
+ * B*(S+8)*(n_heads + 2*n_kv_heads)*head_dim < 2^31 (DCL_E_UNSUPPORTED otherwise). */
 dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
                             const int32_t* p, int32_t gen_end, const dcl_kv* kv, uint32_t flags,
                             dcl_row_stats out, void* ws, size_t ws_bytes, hipStream_t stream);

@@ -189,6 +189,8 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   if (!tokens) return fail(DCL_E_ARG, "tokens is NULL");
   if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
   if ((long)B * S > (1 << 22)) return fail(DCL_E_ARG, "B*S = %ld too large", (long)B * S);
+  if ((long)B * (S + 8) * m->qkv_rows() >= (1L << 31))  // the QKV epilogue addresses q/k/v^T with 32 bits
+    return fail(DCL_E_UNSUPPORTED, "B*S = %ld tokens: q/k/v would reach 2^31 elements", (long)B * S);
   const int P = kv ? kv->prefix_len : 0;
   if (kv) {
     if (!kv->k || !kv->v) return fail(DCL_E_ARG, "kv->k / kv->v is NULL");

@@ -72,7 +72,7 @@ int main(int argc, char** argv) {
         const bf16_t* Wr = W + (size_t)(rot++ % ncopy) * wsz;
         if (s.kind == 'q') {
           QkvOut o{q, k, vt, nullptr, rope, s.H, s.Hkv, 128, S, (S + 7) / 8 * 8, 0};
-          run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiQkv{o}, 0);
+          run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiQkv<128>{o}, 0);
         } else if (s.kind == 's') {
           run_plan(p, Wr, X, s.N, s.T, s.K, nullptr, EpiSwiglu{a}, 0);
         } else if (s.kind == 'r') {

@@ -80,13 +80,16 @@ struct EpiSwiglu {
   }
 };
 
+// Offsets are 32-bit element counts: gemm_qkv rejects outputs of 2^31 elements or more.
+template <int DH>
 struct EpiQkv {
   QkvOut o;
   static constexpr bool kPartial = false;
   template <int SW, int ST>
   __device__ __forceinline__ void apply(f32x4_t (&acc)[SW][ST], int wb, int tb, int lane, int Nw, int T, int, int) const {
-    const int dh = o.dh, half = dh >> 1;
-    const int qrows = o.H * dh, krows = o.Hkv * dh;
+    constexpr int HALF = DH / 2, LOG2DH = DH == 128 ? 7 : 6;
+    static_assert(DH == 64 || DH == 128, "head_dim");
+    const int qrows = o.H * DH, krows = o.Hkv * DH;
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -94,6 +97,11 @@ struct EpiQkv {
       if (t >= T) continue;
       const int b = t / o.S, s = t - b * o.S;
       const int pos = o.pos0 + s;
+      // per token: element offsets of (head 0, position s) in q, k, and of (row 0, key s) in v^T
+      const uint32_t qt = (uint32_t)(b * o.H * o.S + s) * DH;
+      const uint32_t kt = (uint32_t)(b * o.Hkv * o.S + s) * DH;
+      const uint32_t vtt = (uint32_t)b * o.Hkv * DH * o.Sp + s;
+      const float2* rope_t = o.rope ? o.rope + (size_t)pos * HALF : nullptr;
 #pragma unroll
       for (int i = 0; i < SW; ++i) {
         const int w = wq + 16 * i;
@@ -105,28 +113,26 @@ struct EpiQkv {
         if (w < qrows + krows) {
           const bool isq = w < qrows;
           const int wl = isq ? w : w - qrows;
-          const int head = wl / dh, pi = wl - head * dh, jp = pi >> 1;  // pairs (v0,v1) -> jp, (v2,v3) -> jp+1
-          if (o.rope) {
-            const float2 cs0 = o.rope[(size_t)pos * half + jp], cs1 = o.rope[(size_t)pos * half + jp + 1];
+          const int head = wl >> LOG2DH, jp = (wl & (DH - 1)) >> 1;  // pairs (v0,v1) -> jp, (v2,v3) -> jp+1
+          if (rope_t) {
+            const float2 cs0 = rope_t[jp], cs1 = rope_t[jp + 1];
             const float a0 = v0 * cs0.x - v1 * cs0.y, b0 = v1 * cs0.x + v0 * cs0.y;
             const float a1 = v2 * cs1.x - v3 * cs1.y, b1 = v3 * cs1.x + v2 * cs1.y;
             v0 = a0; v1 = b0; v2 = a1; v3 = b1;
           }
-          bf16_t* base = isq ? o.q + (((size_t)b * o.H + head) * o.S + s) * dh
-                             : o.k + (((size_t)b * o.Hkv + head) * o.S + s) * dh;
+          bf16_t* base = isq ? o.q + qt + (uint32_t)head * o.S * DH : o.k + kt + (uint32_t)head * o.S * DH;
           *reinterpret_cast<uint32_t*>(base + jp) = f2bf2(v0, v2);
-          *reinterpret_cast<uint32_t*>(base + half + jp) = f2bf2(v1, v3);
+          *reinterpret_cast<uint32_t*>(base + HALF + jp) = f2bf2(v1, v3);
         } else {
-          const int wl = w - qrows - krows;
-          const int head = wl / dh, dd = wl - head * dh;
-          bf16_t* base = o.vt + (((size_t)b * o.Hkv + head) * dh + dd) * o.Sp + s;
+          const int wl = w - qrows - krows;  // = head * DH + dimension
+          bf16_t* base = o.vt + vtt + (uint32_t)wl * o.Sp;
           base[0] = f2bf(v0);
           base[o.Sp] = f2bf(v1);
-          base[2 * (size_t)o.Sp] = f2bf(v2);
-          base[3 * (size_t)o.Sp] = f2bf(v3);
+          base[2 * o.Sp] = f2bf(v2);
+          base[3 * o.Sp] = f2bf(v3);
           if (s == o.S - 1) {  // the last token also clears the padding keys [S, Sp) of its four rows
             for (int z = 1; s + z < o.Sp; ++z)
-              for (int rr = 0; rr < 4; ++rr) base[rr * (size_t)o.Sp + z] = 0;
+              for (int rr = 0; rr < 4; ++rr) base[rr * o.Sp + z] = 0;
           }
         }
       }
@@ -757,7 +763,9 @@ static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw
 }
 
 void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, hipStream_t s) {
-  run_plan(plan_gemm(Nw, T, K, 0, 1), W, X, Nw, T, K, nullptr, EpiQkv{o}, s);
+  const GemmPlan p = plan_gemm(Nw, T, K, 0, 1);
+  if (o.dh == 128) run_plan(p, W, X, Nw, T, K, nullptr, EpiQkv<128>{o}, s);
+  else run_plan(p, W, X, Nw, T, K, nullptr, EpiQkv<64>{o}, s);
 }
 int gemm_resid(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, float* r, float* P, hipStream_t s) {
   const GemmPlan p = plan_gemm(Nw, T, K, 0, P ? kMaxSplit : 1);
