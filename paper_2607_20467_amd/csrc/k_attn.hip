@@ -60,8 +60,9 @@ __device__ __forceinline__ void attn_wait_stages(int newer) {
 
 // K and V^T tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 into a STAGES-deep ring (no
 // register staging, no padding). K rows (DH/8 chunks of 16 bytes) are XOR-swizzled by the key
-// index, V^T rows (KT/8 chunks of 8 keys) by the dimension index, so the fragment reads below are
-// bank-conflict free. Chunks past the last key read a zero chunk.
+// index, V^T rows (KT/8 chunks of 8 keys) by the dimension index. The 16-byte K fragment reads are
+// bank-conflict free; the 8-byte V^T reads see two-way conflicts (the 16 lanes of a pass read the
+// same half of 8 distinct chunks). Chunks past the last key repeat real data (see below).
 //
 // Key groups: the NQ * KG waves of a workgroup are NQ query waves (16 queries each) times KG key
 // groups. Step t of the ring holds the KG key tiles t*KG .. t*KG + KG - 1; key group g works on
@@ -122,7 +123,9 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   f32x4_t o[DH / 16];
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m = -INFINITY, l = 0.f;  // running max (log2 units, scaled) and sum of this wave's queries
+  // per query: reference point m (log2 units, scaled; within 2^8 of the running maximum, see the
+  // lazy rescaling below) and the sum l of exp2(score - m)
+  float m = -INFINITY, l = 0.f;
   const float scale = a.scale_log2;
 
   // DMA assignment: instruction i of wave w fills the 64-chunk block b = i * NWAVE + w of a ring
@@ -157,139 +160,138 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   const int vlast_f = (S - 1) & ~7;                          // the same for the fresh values alone
   // the main loop below is instantiated twice: without (kFresh) and with a cached prefix
   auto main_loop = [&](auto fresh_only) {
-  constexpr bool kFresh = decltype(fresh_only)::value;
-  auto issue = [&](int t) {
-    const uint32_t stage = lds_base + (uint32_t)((t % STAGES) * SCH) * 16u;
+    constexpr bool kFresh = decltype(fresh_only)::value;
+    auto issue = [&](int t) {
+      const uint32_t stage = lds_base + (uint32_t)((t % STAGES) * SCH) * 16u;
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const bool isk = (i * NWAVE) % TB < KCH / 64;
-      const int mult = isk ? DH : 1;
-      const int k0 = (t * KG + (i * NWAVE) / TB) * KT;
-      const int j = k0 + jrel[i];
-      const void* src;
-      if constexpr (kFresh) {
-        const int jc = min(j, isk ? klast : vlast);
-        src = fsrc[i] + (ptrdiff_t)(jc - jrel[i]) * mult;
-      } else {
-        // fresh side with the same clamping as above, in fresh-key indices; the cache side holds
-        // keys j < P (P is a multiple of 8, so no 8-key chunk straddles the two)
-        const int jf = min(j - P, isk ? klast - P : vlast_f);
-        const bf16_t* fp = fsrc[i] + (ptrdiff_t)(jf - jrel[i]) * mult;
-        const bf16_t* cp = (isk ? kc : vc) + offc[i] + (ptrdiff_t)k0 * mult;
-        src = j < P ? cp : fp;
+      for (int i = 0; i < IPW; ++i) {
+        const bool isk = (i * NWAVE) % TB < KCH / 64;
+        const int mult = isk ? DH : 1;
+        const int k0 = (t * KG + (i * NWAVE) / TB) * KT;
+        const int j = k0 + jrel[i];
+        const void* src;
+        if constexpr (kFresh) {
+          const int jc = min(j, isk ? klast : vlast);
+          src = fsrc[i] + (ptrdiff_t)(jc - jrel[i]) * mult;
+        } else {
+          // fresh side with the same clamping as above, in fresh-key indices; the cache side holds
+          // keys j < P (P is a multiple of 8, so no 8-key chunk straddles the two)
+          const int jf = min(j - P, isk ? klast - P : vlast_f);
+          const bf16_t* fp = fsrc[i] + (ptrdiff_t)(jf - jrel[i]) * mult;
+          const bf16_t* cp = (isk ? kc : vc) + offc[i] + (ptrdiff_t)k0 * mult;
+          src = j < P ? cp : fp;
+        }
+        dma16_at(src, stage + (uint32_t)(i * NWAVE) * 1024u);
       }
-      dma16_at(src, stage + (uint32_t)(i * NWAVE) * 1024u);
-    }
-  };
-
+    };
 
 #pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < nsteps) issue(st);
-  for (int t = 0; t < nsteps; ++t) {
-    // step t landed; the steps t + 1 .. min(nsteps - 1, t + STAGES - 2) may still fly
-    attn_wait_stages<IPW, STAGES - 2>(min(STAGES - 2, nsteps - 1 - t));
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (t + STAGES - 1 < nsteps) issue(t + STAGES - 1);
-    const int k0 = (t * KG + kg) * KT;
-    if (k0 >= nkeys) continue;  // this group's tile is past the end (uniform per wave)
-    const uint4* sK = sm + (t % STAGES) * SCH + kg * TCH;
-    const uint4* sV = sK + KCH;
+    for (int st = 0; st < STAGES - 1; ++st)
+      if (st < nsteps) issue(st);
+    for (int t = 0; t < nsteps; ++t) {
+      // step t landed; the steps t + 1 .. min(nsteps - 1, t + STAGES - 2) may still fly
+      attn_wait_stages<IPW, STAGES - 2>(min(STAGES - 2, nsteps - 1 - t));
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if (t + STAGES - 1 < nsteps) issue(t + STAGES - 1);
+      const int k0 = (t * KG + kg) * KT;
+      if (k0 >= nkeys) continue;  // this group's tile is past the end (uniform per wave)
+      const uint4* sK = sm + (t % STAGES) * SCH + kg * TCH;
+      const uint4* sV = sK + KCH;
 
-    // S^T = K Q^T: lane holds keys 16 kt + 4 lg + r of query lq. The tile's K fragments are read
-    // first and the independent accumulation chains interleaved.
-    bf16x8_t kfr[KT / 16][DH / 32];
+      // S^T = K Q^T: lane holds keys 16 kt + 4 lg + r of query lq. The tile's K fragments are read
+      // first and the independent accumulation chains interleaved.
+      bf16x8_t kfr[KT / 16][DH / 32];
 #pragma unroll
-    for (int kt = 0; kt < KT / 16; ++kt) {
-      const int row = 16 * kt + lq;
+      for (int kt = 0; kt < KT / 16; ++kt) {
+        const int row = 16 * kt + lq;
 #pragma unroll
-      for (int ks = 0; ks < DH / 32; ++ks) {
-        const int c = 4 * ks + lg;
-        kfr[kt][ks] = __builtin_bit_cast(bf16x8_t, sK[row * KC + (c ^ (row & (KC - 1)))]);
+        for (int ks = 0; ks < DH / 32; ++ks) {
+          const int c = 4 * ks + lg;
+          kfr[kt][ks] = __builtin_bit_cast(bf16x8_t, sK[row * KC + (c ^ (row & (KC - 1)))]);
+        }
       }
-    }
-    f32x4_t sc[KT / 16];
+      f32x4_t sc[KT / 16];
 #pragma unroll
-    for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < DH / 32; ++ks)
+      for (int ks = 0; ks < DH / 32; ++ks)
 #pragma unroll
-      for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = mfma16a(kfr[kt][ks], qf[ks], sc[kt]);
-    // V^T fragments, read while the softmax below runs: dimension 16 dt + lq at the keys
-    // 32 s2 + 4 lg + {0..3} and 32 s2 + 16 + 4 lg + {0..3} (the order in which the score MFMA left
-    // the probabilities in the lanes)
-    bf16x8_t vfr[KT / 32][DH / 16];
+        for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = mfma16a(kfr[kt][ks], qf[ks], sc[kt]);
+      // V^T fragments, read while the softmax below runs: dimension 16 dt + lq at the keys
+      // 32 s2 + 4 lg + {0..3} and 32 s2 + 16 + 4 lg + {0..3} (the order in which the score MFMA left
+      // the probabilities in the lanes)
+      bf16x8_t vfr[KT / 32][DH / 16];
 #pragma unroll
-    for (int s2 = 0; s2 < KT / 32; ++s2) {
-      const int c0 = 4 * s2 + (lg >> 1), c1 = c0 + 2, half = lg & 1;
+      for (int s2 = 0; s2 < KT / 32; ++s2) {
+        const int c0 = 4 * s2 + (lg >> 1), c1 = c0 + 2, half = lg & 1;
 #pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) {
-        const int d = 16 * dt + lq;
-        const uint2 v0 = reinterpret_cast<const uint2*>(sV + d * VC + (c0 ^ (d & (VC - 1))))[half];
-        const uint2 v1 = reinterpret_cast<const uint2*>(sV + d * VC + (c1 ^ (d & (VC - 1))))[half];
-        vfr[s2][dt] = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+        for (int dt = 0; dt < DH / 16; ++dt) {
+          const int d = 16 * dt + lq;
+          const uint2 v0 = reinterpret_cast<const uint2*>(sV + d * VC + (c0 ^ (d & (VC - 1))))[half];
+          const uint2 v1 = reinterpret_cast<const uint2*>(sV + d * VC + (c1 ^ (d & (VC - 1))))[half];
+          vfr[s2][dt] = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+        }
       }
-    }
-    if (k0 + KT > nkeys) {  // only the last tile holds keys past the end
+      if (k0 + KT > nkeys) {  // only the last tile holds keys past the end
+#pragma unroll
+        for (int kt = 0; kt < KT / 16; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (k0 + 16 * kt + 4 * lg + r >= nkeys) sc[kt][r] = -INFINITY;
+      }
+      float tmax = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < KT / 16; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (k0 + 16 * kt + 4 * lg + r >= nkeys) sc[kt][r] = -INFINITY;
-    }
-    float tmax = -INFINITY;
+        for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, sc[kt][r]);
+      // the four lane groups holding one query's keys: lanes l, l^16, l^32, l^48
+      tmax = xor_lanes16(tmax, [](float x, float y) { return fmaxf(x, y); });
+      tmax = xor_lanes32(tmax, [](float x, float y) { return fmaxf(x, y); });
+      // Lazy rescaling: the reference point m only moves when a score exceeds it by more than
+      // 2^8 (probabilities up to 256 are exact to represent and sum in float32); the division by
+      // the running sum at the end makes the result independent of the reference point. When no
+      // lane of the wave moves, the output rescale is skipped.
+      const float ts = tmax * scale;
+      const bool move = ts > m + 8.f;  // true on the first processed tile (m = -inf)
+      const float mn = move ? ts : m;
+      float psum = 0.f;
 #pragma unroll
-    for (int kt = 0; kt < KT / 16; ++kt)
+      for (int kt = 0; kt < KT / 16; ++kt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, sc[kt][r]);
-    // the four lane groups holding one query's keys: lanes l, l^16, l^32, l^48
-    tmax = xor_lanes16(tmax, [](float x, float y) { return fmaxf(x, y); });
-    tmax = xor_lanes32(tmax, [](float x, float y) { return fmaxf(x, y); });
-    // Lazy rescaling: the reference point m only moves when a score exceeds it by more than
-    // 2^8 (probabilities up to 256 are exact to represent and sum in float32); the division by
-    // the running sum at the end makes the result independent of the reference point. When no
-    // lane of the wave moves, the output rescale is skipped.
-    const float ts = tmax * scale;
-    const bool move = ts > m + 8.f;  // true on the first processed tile (m = -inf)
-    const float mn = move ? ts : m;
-    float psum = 0.f;
+        for (int r = 0; r < 4; ++r) {
+          const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], scale, -mn));
+          sc[kt][r] = pv;
+          psum += pv;
+        }
+      psum = xor_lanes16(psum, [](float x, float y) { return x + y; });
+      psum = xor_lanes32(psum, [](float x, float y) { return x + y; });
+      if (__builtin_amdgcn_ballot_w64(move)) {
+        const float alpha = __builtin_amdgcn_exp2f(m - mn);  // 1 in the lanes that keep m
+        l *= alpha;
 #pragma unroll
-    for (int kt = 0; kt < KT / 16; ++kt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], scale, -mn));
-        sc[kt][r] = pv;
-        psum += pv;
+        for (int dt = 0; dt < DH / 16; ++dt) o[dt] *= alpha;
       }
-    psum = xor_lanes16(psum, [](float x, float y) { return x + y; });
-    psum = xor_lanes32(psum, [](float x, float y) { return x + y; });
-    if (__builtin_amdgcn_ballot_w64(move)) {
-      const float alpha = __builtin_amdgcn_exp2f(m - mn);  // 1 in the lanes that keep m
-      l *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) o[dt] *= alpha;
-    }
-    l += psum;
-    m = mn;
+      l += psum;
+      m = mn;
 
-    // O^T += V^T P^T over 32-key steps; P enters as bf16 hi + lo parts
+      // O^T += V^T P^T over 32-key steps; P enters as bf16 hi + lo parts
 #pragma unroll
-    for (int s2 = 0; s2 < KT / 32; ++s2) {
-      uint32_t hi[4], lo[4];
+      for (int s2 = 0; s2 < KT / 32; ++s2) {
+        uint32_t hi[4], lo[4];
 #pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const float p0 = sc[2 * s2 + (x >> 1)][(x & 1) * 2], p1 = sc[2 * s2 + (x >> 1)][(x & 1) * 2 + 1];
-        hi[x] = f2bf2(p0, p1);
-        lo[x] = f2bf2(p0 - __uint_as_float(hi[x] << 16), p1 - __uint_as_float(hi[x] & 0xFFFF0000u));
+        for (int x = 0; x < 4; ++x) {
+          const float p0 = sc[2 * s2 + (x >> 1)][(x & 1) * 2], p1 = sc[2 * s2 + (x >> 1)][(x & 1) * 2 + 1];
+          hi[x] = f2bf2(p0, p1);
+          lo[x] = f2bf2(p0 - __uint_as_float(hi[x] << 16), p1 - __uint_as_float(hi[x] & 0xFFFF0000u));
+        }
+        const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+        const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+#pragma unroll
+        for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], phi, o[dt]);
+#pragma unroll
+        for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], plo, o[dt]);
       }
-      const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
-      const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], phi, o[dt]);
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], plo, o[dt]);
     }
-  }
 
   };
   if (P == 0) main_loop(std::integral_constant<bool, true>{});
