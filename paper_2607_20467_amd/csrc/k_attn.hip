@@ -9,8 +9,10 @@
 // in registers), so each lane holds 16 scores of ONE query. Its softmax probabilities then feed the
 // P*V product directly as the MFMA B operand of O^T = V^T P^T, with V^T read from a key-contiguous
 // LDS tile in the matching key order; no register shuffle of P is needed.
-// P is split into bf16 hi + lo parts (two MFMAs), so the probabilities enter the product with
-// ~16 significant bits instead of 8.
+// P is split into three bf16 parts (hi + mid + lo, three MFMAs), so the probabilities enter the
+// product with at least 24 significant bits, as in a float32 evaluation. Two parts (16 bits) were
+// measurably less accurate than float32: on sequences of 5-8 tokens they flipped the bf16 rounding
+// of about a quarter of the final hidden states of a small model against a float64 reference.
 #include <type_traits>
 
 #include "dcl_internal.h"
@@ -274,20 +276,25 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
       l += psum;
       m = mn;
 
-      // O^T += V^T P^T over 32-key steps; P enters as bf16 hi + lo parts
+      // O^T += V^T P^T over 32-key steps; P enters as three bf16 parts (hi + mid + lo)
 #pragma unroll
       for (int s2 = 0; s2 < KT / 32; ++s2) {
-        uint32_t hi[4], lo[4];
+        uint32_t hi[4], mi[4], lo[4];
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           const float p0 = sc[2 * s2 + (x >> 1)][(x & 1) * 2], p1 = sc[2 * s2 + (x >> 1)][(x & 1) * 2 + 1];
           hi[x] = f2bf2(p0, p1);
-          lo[x] = f2bf2(p0 - __uint_as_float(hi[x] << 16), p1 - __uint_as_float(hi[x] & 0xFFFF0000u));
+          const float r0 = p0 - __uint_as_float(hi[x] << 16), r1 = p1 - __uint_as_float(hi[x] & 0xFFFF0000u);
+          mi[x] = f2bf2(r0, r1);
+          lo[x] = f2bf2(r0 - __uint_as_float(mi[x] << 16), r1 - __uint_as_float(mi[x] & 0xFFFF0000u));
         }
         const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+        const bf16x8_t pmi = __builtin_bit_cast(bf16x8_t, make_uint4(mi[0], mi[1], mi[2], mi[3]));
         const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
         for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], phi, o[dt]);
+#pragma unroll
+        for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], pmi, o[dt]);
 #pragma unroll
         for (int dt = 0; dt < DH / 16; ++dt) o[dt] = mfma16a(vfr[s2][dt], plo, o[dt]);
       }
@@ -368,9 +375,9 @@ static void run_attn(const AttnArgs& a, hipStream_t s) {
 // A two-stage ring of 64-key tiles. Few query waves (B * H * S / 16 below 4096): 4 query waves
 // x 2 key groups per workgroup, so each wave walks half the keys and twice as many waves share a
 // CU; many query waves: 8 query waves x 1 group, whose 64 KB ring lets two workgroups share a CU.
-// Measured on MI355X (LLaDA-8B / Dream-7B heads): 384 tokens 13.0 us (18.2 with one group of 4),
-// 1280 tokens 90 us (98 with one group of 8), 8 x 64 tokens over a 1216-key cache 33 us (49 with
-// one group of 4), Dream-7B 4 x 768 tokens 95 us (119 with two groups of 4).
+// Measured on MI355X (LLaDA-8B / Dream-7B heads, three-part P): 384 tokens 12.3 us (17.6 with one
+// group of 8), 1280 tokens 89 us (99 with one group of 8), 8 x 64 tokens over a 1216-key cache
+// 36 us (54 with one group of 8), Dream-7B 4 x 768 tokens 100 us (117 with two groups of 4).
 void launch_attention(const AttnArgs& a, hipStream_t s) {
   const long query_waves = (long)a.B * a.H * ((a.S + 15) / 16);
   if (query_waves >= 4096) run_attn<8, 1, 64, 2>(a, s);

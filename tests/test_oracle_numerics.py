@@ -188,3 +188,22 @@ def test_kv_prefix_forward_equals_full_forward(tiny_weights):
     cache = [(k[:, :P], v[:, :, :P]) for k, v in kvs]
     part = oracle.forward(w.geom, W, tok[0, P:], P + np.arange(w.seq - P), kv=lambda l: cache[l])
     np.testing.assert_array_equal(part, full[P:])
+
+
+def test_coordinate_permutation_is_a_symmetry(tiny_weights):
+    """The whole-step tolerance samples float32 summation orders by permuting the model's d_model and
+    d_ffn coordinates. That must be an exact symmetry: the permuted model's hidden states are the
+    plain model's with their coordinates permuted, and its step statistics are the same."""
+    from helpers import permuted_weights
+    w, stored, W = tiny_weights("c1")
+    tok, p = synth.initial_state(w)
+    pos = np.arange(w.seq)
+    Wp = permuted_weights(WeightView(stored, bf16_boundary=False), w.geom, 5)
+    pd = np.random.default_rng(5).permutation(w.geom.d_model)
+    a = oracle.forward(w.geom, WeightView(stored, bf16_boundary=False), tok[0], pos, bf16_boundary=False)
+    b = oracle.forward(w.geom, Wp, tok[0], pos, bf16_boundary=False)
+    np.testing.assert_allclose(b, a[:, pd], rtol=1e-10, atol=1e-12)
+    s0 = oracle.step(w.geom, W, tok, p, w.gen_end)
+    s1 = oracle.step(w.geom, permuted_weights(W, w.geom, 5), tok, p, w.gen_end)
+    np.testing.assert_array_equal(s0["top1"], s1["top1"])
+    np.testing.assert_allclose(s0["conf"], s1["conf"], rtol=1e-9, atol=1e-12)
