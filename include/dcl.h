@@ -114,7 +114,9 @@ const char* dcl_status_string(dcl_status s);
 /* Detail of the last non-OK status returned on this thread (empty string if none). */
 const char* dcl_last_error(void);
 
-/* Validate `cfg` (host) and create a handle. *out receives the handle (host). */
+/* Validate `cfg` (host) and create a handle. *out receives the handle (host). Every weight matrix
+ * (vocab x d_model, (n_heads + 2*n_kv_heads)*head_dim x d_model, 2*d_ffn x d_model, ...) must hold
+ * fewer than 2^31 elements (DCL_E_UNSUPPORTED otherwise). */
 dcl_status dcl_model_create(const dcl_config* cfg, dcl_model_t* out);
 
 /* Release the handle (host memory only; the weight buffer stays the caller's). NULL is a no-op. */
@@ -147,8 +149,10 @@ size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_p
  * memory. Token i is at absolute position kv_prefix + i; with kv == NULL the forward covers the
  * S tokens alone, otherwise they also attend to the cached prefix. Token ids outside
  * [0, vocab) read an all-zero embedding row. Writes `out` (all B*S rows). ws: device,
- * ws_bytes >= dcl_workspace_bytes(model, B, S, prefix), 256-byte aligned. Sizes: B*S <= 2^22 and
- * B*(S+8)*(n_heads + 2*n_kv_heads)*head_dim < 2^31 (DCL_E_UNSUPPORTED otherwise). */
+ * ws_bytes >= dcl_workspace_bytes(model, B, S, prefix), 256-byte aligned. Sizes: B*S <= 2^22
+ * (DCL_E_ARG otherwise), B*(S+8)*(n_heads + 2*n_kv_heads)*head_dim < 2^31 and
+ * B*S*max(d_model, n_heads*head_dim, d_ffn) < 2^31 (DCL_E_UNSUPPORTED otherwise: the kernels
+ * address q/k/v^T and the GEMM operands with 32-bit offsets). */
 dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
                             const int32_t* p, int32_t gen_end, const dcl_kv* kv, uint32_t flags,
                             dcl_row_stats out, void* ws, size_t ws_bytes, hipStream_t stream);
@@ -219,7 +223,8 @@ size_t dcl_score_workspace_bytes(dcl_model_t model, int32_t n);
  * Eq. threshold_pd) on given final hidden states: hidden bf16 [n, d_model] (device, 16-byte
  * aligned), already final-normalised. Writes statistics for rows 0..n-1 into `out` (each array
  * has n entries). Logits are never written to memory. ws: device, 256-byte aligned,
- * ws_bytes >= dcl_score_workspace_bytes(model, n). */
+ * ws_bytes >= dcl_score_workspace_bytes(model, n). Sizes: 1 <= n <= 2^22 (DCL_E_ARG otherwise)
+ * and n*d_model < 2^31 (DCL_E_UNSUPPORTED otherwise). */
 dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dcl_row_stats out,
                             void* ws, size_t ws_bytes, hipStream_t stream);
 

@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -51,6 +52,12 @@ dcl_status check_config(const dcl_config* c) {
     return fail(DCL_E_ARG, "max_positions %d outside [1, 65536]", c->max_positions);
   if (c->qkv_bias != 0 && c->qkv_bias != 1) return fail(DCL_E_ARG, "qkv_bias must be 0 or 1");
   if (c->rope_enabled != 0 && c->rope_enabled != 1) return fail(DCL_E_ARG, "rope_enabled must be 0 or 1");
+  // the GEMM kernels form operand offsets (row * K) in 32 bits: every weight matrix stays below 2^31 elements
+  const long d = c->d_model, hd = (long)c->n_heads * c->head_dim;
+  const long qkv = (long)(c->n_heads + 2 * c->n_kv_heads) * c->head_dim;
+  const long biggest = std::max({(long)c->vocab * d, qkv * d, hd * d, 2L * c->d_ffn * d});
+  if (biggest >= (1L << 31))
+    return fail(DCL_E_UNSUPPORTED, "a weight matrix of %ld elements: the kernels address at most 2^31", biggest);
   return DCL_OK;
 }
 
@@ -191,6 +198,11 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   if ((long)B * S > (1 << 22)) return fail(DCL_E_ARG, "B*S = %ld too large", (long)B * S);
   if ((long)B * (S + 8) * m->qkv_rows() >= (1L << 31))  // the QKV epilogue addresses q/k/v^T with 32 bits
     return fail(DCL_E_UNSUPPORTED, "B*S = %ld tokens: q/k/v would reach 2^31 elements", (long)B * S);
+  // the GEMMs address their activation operand ([tokens, K], K up to max(d_model, H*dh, d_ffn)) with 32 bits
+  const long kmax = std::max({(long)m->cfg.d_model, (long)m->cfg.n_heads * m->cfg.head_dim, (long)m->cfg.d_ffn});
+  if ((long)B * S * kmax >= (1L << 31))
+    return fail(DCL_E_UNSUPPORTED, "B*S = %ld tokens: a GEMM activation operand would reach 2^31 elements",
+                (long)B * S);
   const int P = kv ? kv->prefix_len : 0;
   if (kv) {
     if (!kv->k || !kv->v) return fail(DCL_E_ARG, "kv->k / kv->v is NULL");
@@ -668,6 +680,9 @@ dcl_status dcl_score_hidden(dcl_model_t model, const void* hidden, int32_t n, dc
   if (!hidden) return fail(DCL_E_ARG, "hidden is NULL");
   if ((reinterpret_cast<uintptr_t>(hidden) & 15) != 0) return fail(DCL_E_ARG, "hidden must be 16-byte aligned");
   if (n < 1 || n > (1 << 22)) return fail(DCL_E_ARG, "n=%d outside [1, 2^22]", n);
+  if ((long)n * m->cfg.d_model >= (1L << 31))
+    return fail(DCL_E_UNSUPPORTED, "n=%d rows of %d: the LM-head GEMM addresses at most 2^31 elements", n,
+                m->cfg.d_model);
   if (!out.top1 || !out.top2 || !out.conf || !out.p2 || !out.lse) return fail(DCL_E_ARG, "an output array is NULL");
   if (!ws) return fail(DCL_E_ARG, "workspace is NULL");
   if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(DCL_E_ARG, "workspace must be 256-byte aligned");

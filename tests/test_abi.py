@@ -46,13 +46,19 @@ def _cfg(dcl, **kw):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 96, 2), ("n_kv_heads", 5, 2), ("d_model", 4100, 2), ("d_model", 8208, 2), ("d_ffn", 8, 2), ("vocab", 1, 1),
     ("mask_id", 126464, 1), ("mask_id", -1, 1), ("rms_eps", 0.0, 1), ("rope_base", 1.0, 1),
-    ("max_positions", 0, 1), ("n_layers", 0, 1), ("qkv_bias", 2, 1)])
+    ("max_positions", 0, 1), ("n_layers", 0, 1), ("qkv_bias", 2, 1),
+    ("vocab", 524288, 2), ("d_ffn", 262144, 2)])   # a weight matrix of 2^31 elements (LM head, gate||up)
 def test_model_create_rejects(dcl, field, value, status):
     with pytest.raises(dcl.DclError) as e:
         dcl.dcl_model_create(_cfg(dcl, **{field: value}))
     assert e.value.status == status
     assert dcl.dcl_last_error()
     assert dcl.dcl_weights_bytes(_cfg(dcl, **{field: value})) == 0
+
+
+def test_model_create_accepts_weight_matrices_just_below_2_31(dcl):
+    m = dcl.dcl_model_create(_cfg(dcl, vocab=524287, d_ffn=262128))
+    dcl.dcl_model_destroy(m)
 
 
 def test_sizes(dcl):
