@@ -33,7 +33,7 @@ def _setup(key, gen_len=48, batch=None):
     return w, run, x, p
 
 
-def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0):
+def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0, kv=None):
     """States after each of n_iter eager iterations (device-resident, synchronised between them)."""
     import torch
     import paper_2607_20467_amd as dcl
@@ -49,14 +49,15 @@ def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0):
     ke = torch.zeros(B, dtype=torch.int32, device="cuda")
     out = []
     for _ in range(n_iter):
-        run.step(tok, p, S, stats=st, flags=score_flags)
+        run.step(tok, p, S, stats=st, flags=score_flags, kv=kv)
         dcl.dcl_select_contiguous(tok, B, S, p, S, L, tc, td, w.geom.mask_id, st, kr, ke, select_flags)
         torch.cuda.synchronize()
         out.append((tok.cpu().numpy(), p.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()))
     return out
 
 
-def _generate(run, w, x0, p0, L, tc, td, max_steps, check_every=1, score_flags=0, select_flags=0, hist=None):
+def _generate(run, w, x0, p0, L, tc, td, max_steps, check_every=1, score_flags=0, select_flags=0, hist=None,
+              kv=None):
     import torch
     import paper_2607_20467_amd as dcl
     B, S = x0.shape
@@ -64,8 +65,8 @@ def _generate(run, w, x0, p0, L, tc, td, max_steps, check_every=1, score_flags=0
     st = run.new_stats(B, S)
     kr = torch.zeros(B, dtype=torch.int32, device="cuda")
     ke = torch.zeros(B, dtype=torch.int32, device="cuda")
-    ws, n = run.workspace(B, S)
-    steps = dcl.dcl_generate(run.model, tok, B, S, p, S, None, score_flags, L, tc, td, select_flags, max_steps,
+    ws, n = run.workspace(B, S, 0 if kv is None else kv[2])
+    steps = dcl.dcl_generate(run.model, tok, B, S, p, S, kv, score_flags, L, tc, td, select_flags, max_steps,
                              check_every, st, kr, ke, hist, ws, n)
     torch.cuda.synchronize()
     return steps, tok.cpu().numpy(), p.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()
@@ -143,3 +144,37 @@ def test_score_all_mode_replays_match():
     assert steps == 6
     np.testing.assert_array_equal(tok, ref[-1][0])
     np.testing.assert_array_equal(p, ref[-1][1])
+
+
+def test_cached_prefix_replays_match_the_eager_loop():
+    """The prompt's keys/values go into a cache once (dcl_kv_append); the loop then forwards only the
+    generation region, which attends to [cached prompt || itself] (the prefix-KV decode mode)."""
+    import torch
+    w, run, x0, p0 = _setup("c1s")
+    g = w.geom
+    B, N = x0.shape[0], int(p0[0])
+    assert N % 8 == 0
+    ks = [torch.zeros((B, g.n_kv_heads, N, g.head_dim), dtype=torch.int16, device="cuda") for _ in range(g.n_layers)]
+    vs = [torch.zeros((B, g.n_kv_heads, g.head_dim, N), dtype=torch.int16, device="cuda") for _ in range(g.n_layers)]
+    run.kv_append(to_dev(np.ascontiguousarray(x0[:, :N])), (ks, vs, 0, N))
+    kv = (ks, vs, N, N)
+    x = np.ascontiguousarray(x0[:, N:])
+    p = np.zeros(B, np.int32)
+    S = x.shape[1]
+    L, tc, td = 16, 0.7, 0.9
+    ref = _eager(run, w, x, p, L, tc, td, 48, kv=kv)
+    n_done = next(i + 1 for i, (_, pk, _, _) in enumerate(ref) if (pk >= S).all())
+    print("cached-prefix eager loop finished in", n_done, "iterations", flush=True)
+    for k in sorted({1, 2, 3, n_done}):
+        steps, tok, pk, kr, ke = _generate(run, w, x, p, L, tc, td, max_steps=k, kv=kv)
+        assert steps == k
+        rt, rp, rkr, rke = ref[k - 1]
+        np.testing.assert_array_equal(tok, rt, err_msg=f"tokens after {k} iterations")
+        np.testing.assert_array_equal(pk, rp, err_msg=f"p after {k} iterations")
+        np.testing.assert_array_equal(kr, rkr, err_msg=f"K_raw after {k} iterations")
+        np.testing.assert_array_equal(ke, rke, err_msg=f"K_eff after {k} iterations")
+    # the cache is read, never written, by the loop
+    ks2 = [k.clone() for k in ks]
+    _generate(run, w, x, p, L, tc, td, max_steps=1000, kv=kv)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(ks, ks2))
