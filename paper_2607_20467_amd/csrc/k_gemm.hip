@@ -631,7 +631,8 @@ static const TileCfg kCfgs[] = {
     {128, 128, 128, 2, 2, 4, 0}, {64, 192, 128, 2, 2, 4, 0},  {128, 192, 128, 2, 4, 4, 0},
     {128, 128, 64, 3, 2, 4, 0},  {128, 256, 64, 3, 2, 8, 0},  {128, 192, 64, 3, 2, 4, 0},
     {128, 256, 64, 2, 2, 8, 0},  {256, 256, 64, 2, 2, 4, 0},  {256, 192, 64, 2, 2, 4, 0},
-    {256, 128, 64, 3, 2, 2, 0},  {256, 256, 64, 2, 4, 2, 0},
+    {256, 128, 64, 3, 2, 2, 0},  {256, 256, 64, 2, 4, 2, 0},  {96, 192, 64, 4, 3, 4, 0},
+    {96, 192, 64, 3, 3, 4, 0},   {192, 96, 64, 3, 4, 3, 0},
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kCUs = 256;
@@ -731,6 +732,8 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, epi);
 }
 
+static_assert(kNumCfgs == 26, "run_plan dispatches every configuration of kCfgs");
+
 template <class Epi>
 static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
                      const Epi& epi, hipStream_t s) {
@@ -758,7 +761,10 @@ static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw
     case 19: run_cfg<256, 256, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 20: run_cfg<256, 192, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 21: run_cfg<256, 128, 64, 3, 2, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
-    default: run_cfg<256, 256, 64, 2, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 22: run_cfg<256, 256, 64, 2, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 23: run_cfg<96, 192, 64, 4, 3, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    case 24: run_cfg<96, 192, 64, 3, 3, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
+    default: run_cfg<192, 96, 64, 3, 4, 3>(W, X, Nw, T, K, t_count, n, epi, s); break;
   }
 }
 
