@@ -36,7 +36,8 @@ def is_stale() -> bool:
     if not os.path.exists(LIB):
         return True
     t = os.path.getmtime(LIB)
-    deps = sources() + [os.path.join(CSRC, "dcl_internal.h"), os.path.join(ROOT, "include", "dcl.h")]
+    deps = sources() + [os.path.join(CSRC, "dcl_internal.h"), os.path.join(CSRC, "gemm_tuned.inc"),
+                        os.path.join(ROOT, "include", "dcl.h")]
     return any(os.path.getmtime(p) > t for p in deps)
 
 
