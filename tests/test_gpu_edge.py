@@ -3,8 +3,8 @@
   selection changes nothing;
 * a batch mixing finished and active sequences (one with a single uncommitted position);
 * very short sequences: 8 tokens (one 8-key chunk, a single attention tile whose second key group
-  is empty), 5 tokens (a one-token generation region, S not a multiple of 8) and 2 tokens (one
-  prompt token and one masked position);
+  is empty), 5 tokens (a one-token generation region, S not a multiple of 8), 2 tokens (one
+  prompt token and one masked position) and a single masked token (one key, no prompt);
 * a step whose selection finishes the sequence.
 Statistics are compared within the whole-step tolerance (helpers.py), selections bit-exactly on
 the GPU's own statistics."""
@@ -95,7 +95,7 @@ def test_mixed_finished_and_active():
     assert (t_gpu[2] != w.geom.mask_id).all()
 
 
-@pytest.mark.parametrize("prompt_len,gen_len,window", [(4, 4, 4), (4, 1, 1), (1, 7, 3), (1, 1, 1)])
+@pytest.mark.parametrize("prompt_len,gen_len,window", [(4, 4, 4), (4, 1, 1), (1, 7, 3), (1, 1, 1), (0, 1, 1)])
 def test_short_sequences(prompt_len, gen_len, window):
     w = _workload(f"short_{prompt_len}_{gen_len}", batch=2, prompt_len=prompt_len, gen_len=gen_len,
                   window=window, p=prompt_len, draft=(0, 0))
