@@ -149,3 +149,34 @@ def test_margin_acceptance_bit_exact(seed):
         got = _run_gpu(t, p, end, L, tc, td, mask, top1, conf, flags, p2=p2)
         for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
             np.testing.assert_array_equal(g, r, err_msg=f"{name} flags={flags} B={B} S={S} L={L} end={end}")
+
+
+@pytest.mark.parametrize("tc,L", [(0.0, 1), (0.0, 5000), (1.0, 1), (1.0, 5000), (0.7, 5000)])
+def test_select_degenerate_thresholds_and_windows(tc, L):
+    """tau_c = 0: every scored window row passes, K = L_eff; tau_c = 1: none passes, K = 0 and the
+    progress guard commits one token (K_eff = 1); a window longer than the remaining region is
+    clipped to gen_end - p; L = 1 is the sequential decoder. Bit-exact against the oracle."""
+    rng = np.random.default_rng(int(tc * 10) + L)
+    mask = 4095
+    B, S = 5, 333
+    end = 300
+    tok = rng.integers(0, 4000, (B, S))
+    p = np.array([0, 17, 150, 299, 300])
+    for b in range(B):
+        tok[b, p[b]:] = np.where(rng.random(S - p[b]) < 0.7, mask, tok[b, p[b]:])
+        tok[b, p[b]:min(p[b] + L, end)] = mask
+    sc = scored_mask(tok, p, end, mask, False)
+    conf = np.where(sc, rng.uniform(1e-4, 1, (B, S)).astype(np.float32), np.float32(-1)).astype(np.float32)
+    top1 = np.where(sc, rng.integers(0, 4000, (B, S)), -1)
+    ref = oracle.select_contiguous(tok, p, end, L, tc, 0.98, mask, top1, conf.astype(np.float64))
+    got = _run_gpu(tok, p, end, L, tc, 0.98, mask, top1, conf)
+    for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
+        np.testing.assert_array_equal(g, r, err_msg=f"{name} tc={tc} L={L}")
+    live = p < end
+    l_eff = np.minimum(L, end - p)
+    if tc == 0.0:
+        np.testing.assert_array_equal(got[2][live], l_eff[live])
+    if tc == 1.0:
+        np.testing.assert_array_equal(got[2][live], 0)
+        np.testing.assert_array_equal(got[3][live], 1)
+    np.testing.assert_array_equal(got[1][~live], p[~live])      # a finished sequence does not move
