@@ -269,3 +269,38 @@ def test_entropy_of_steered_and_flat_rows():
     assert H[1] == pytest.approx(np.log(V), rel=1e-12)
     assert abs(st["entropy"][1] - np.log(V)) < 1e-4
     assert abs(st["entropy"][0] - H[0]) < 2 * LOGIT_TOL
+
+
+def test_kv_prefix_step_ragged_gqa_with_spare_capacity():
+    """A 40-key prefix (a 64-key tile then holds cache and fresh keys), 21 fresh tokens (S not a
+    multiple of 8), GQA 4/2 with head_dim 128 and q/k/v bias, and a cache whose capacity (48)
+    exceeds the prefix: the unused positions hold large finite values that must never be read."""
+    import torch
+    base = CASES["gqa_bias_dh128"]
+    w = dataclasses.replace(base, key="kv_ragged", batch=3, prompt_len=0, gen_len=21, window=8, p=0, draft=(8, 16),
+                            kv_prefix=40, kv_seed=5)
+    stored = _setup("gqa_bias_dh128")[1]
+    W = WeightView(stored)
+    run = runner_for(w, stored)
+    g = w.geom
+    caches = [synth.kv_cache_layer(w, l) for l in range(g.n_layers)]
+
+    def kv(b, l):
+        k, v = caches[l]
+        return synth.bf16_bits_to_f32(k[b]), synth.bf16_bits_to_f32(v[b])
+    kv.prefix = w.kv_prefix
+    tok, p = synth.initial_state(w)
+    ref = oracle.step(g, W, tok, p, w.gen_end, kv=kv)
+    ct, lt = derived_tolerance(g, W, tok, p, w.gen_end, ref, kv=kv)
+    cap, P = 48, w.kv_prefix
+    big = np.uint16(0x4700)                          # bf16 32768
+    ks, vs = [], []
+    for k, v in caches:
+        kk = np.full((w.batch, g.n_kv_heads, cap, g.head_dim), big, np.uint16)
+        vv = np.full((w.batch, g.n_kv_heads, g.head_dim, cap), big, np.uint16)
+        kk[:, :, :P] = k
+        vv[:, :, :, :P] = v
+        ks.append(torch.from_numpy(kk.view(np.int16)).cuda())
+        vs.append(torch.from_numpy(vv.view(np.int16)).cuda())
+    st = run.step(to_dev(tok), to_dev(p), w.gen_end, kv=(ks, vs, P, cap))
+    compare_stats(stats_to_np(st), ref, w.tau_commit, w.tau_draft, what="kv-prefix-ragged", conf_tol=ct, logit_tol=lt)
