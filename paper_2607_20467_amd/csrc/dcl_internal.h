@@ -4,9 +4,23 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "dcl.h"
 
 namespace dcl {
+
+// Raise a kernel's dynamic-LDS limit to `bytes` once per device (devices 0-31): the attribute
+// belongs to the device the call is made on, so the first launch on each device sets it and later
+// launches only read the mask. Safe when several host threads launch at once.
+inline void ensure_dynamic_lds(const void* kern, size_t bytes, std::atomic<uint32_t>& devices_done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return;
+  const uint32_t bit = 1u << (dev & 31);
+  if (devices_done.load(std::memory_order_acquire) & bit) return;
+  if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) == hipSuccess)
+    devices_done.fetch_or(bit, std::memory_order_acq_rel);
+}
 
 typedef uint16_t bf16_t;  // bfloat16 bit pattern
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));

@@ -353,21 +353,15 @@ static void run_attn(const AttnArgs& a, hipStream_t s) {
   const size_t lds = (size_t)STAGES * KG * (KT * (a.dh / 8) + a.dh * (KT / 8)) * 16;
   if (a.dh == 128) {
     auto kern = attn_kernel<NQ, KG, KT, 128, STAGES>;
-    static bool set = false;
-    if (!set) {
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      set = true;
-    }
+    static std::atomic<uint32_t> lds_set{0};
+    ensure_dynamic_lds(reinterpret_cast<const void*>(kern), lds, lds_set);
     hipLaunchKernelGGL(kern, grid, dim3(NQ * KG * 64), lds, s, a);
   } else if constexpr ((KT * 8 / 64) % (NQ * KG) != 0 || (64 * (KT / 8) / 64) % (NQ * KG) != 0) {
     run_attn<4, 2, 64, 2>(a, s);  // this wave layout does not tile head_dim 64: the default one does
   } else {
     auto kern = attn_kernel<NQ, KG, KT, 64, STAGES>;
-    static bool set = false;
-    if (!set) {
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      set = true;
-    }
+    static std::atomic<uint32_t> lds_set{0};
+    ensure_dynamic_lds(reinterpret_cast<const void*>(kern), lds, lds_set);
     hipLaunchKernelGGL(kern, grid, dim3(NQ * KG * 64), lds, s, a);
   }
 }

@@ -605,12 +605,8 @@ static void run_rp(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const
   const int grid = 8 * ((units + 7) / 8);
   const size_t lds = (size_t)2 * (BW + BT) * 8 * 16;
   auto kern = gemm_rp_kernel<BW, BT, PF, WW, WT, Epi>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)lds);
-    attr_set = true;
-  }
+  static std::atomic<uint32_t> lds_set{0};
+  ensure_dynamic_lds(reinterpret_cast<const void*>(kern), lds, lds_set);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, epi);
 }
 
@@ -716,19 +712,20 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   if (t_count && grid > 8 * kCUs) grid = 8 * kCUs;
   const size_t lds = (size_t)STAGES * (BW + BT) * (KD / 8) * 16;
   auto kern = gemm_kernel<BW, BT, KD, STAGES, WW, WT, Epi>;
-  static int fits = -1;  // per instantiation: the ring plus the epilogue's static LDS fit in a CU
-  if (fits < 0) {
+  // per instantiation: the ring plus the epilogue's static LDS fit in a CU (-1 = not yet known)
+  static std::atomic<int> fits{-1};
+  if (fits.load(std::memory_order_acquire) < 0) {
     hipFuncAttributes at{};
-    fits = hipFuncGetAttributes(&at, reinterpret_cast<const void*>(kern)) == hipSuccess &&
-           at.sharedSizeBytes + lds <= kLdsBytes;
-    if (fits)
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)lds);
+    fits.store(hipFuncGetAttributes(&at, reinterpret_cast<const void*>(kern)) == hipSuccess &&
+                   at.sharedSizeBytes + lds <= kLdsBytes,
+               std::memory_order_release);
   }
-  if (!fits) {  // never planned (plans respect kLdsBytes); keep a launch the runtime would reject off the GPU
-    run_cfg<128, 128, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, nsplit, epi, s);
+  if (!fits.load(std::memory_order_acquire)) {  // never planned (plans respect kLdsBytes); keep a launch the
+    run_cfg<128, 128, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, nsplit, epi, s);  // runtime would reject off the GPU
     return;
   }
+  static std::atomic<uint32_t> lds_set{0};
+  ensure_dynamic_lds(reinterpret_cast<const void*>(kern), lds, lds_set);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(WW * WT * 64), lds, s, W, X, Nw, T, K, t_count, nsplit, epi);
 }
 
