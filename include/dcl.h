@@ -195,7 +195,9 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
  * replay one iteration captured into a HIP graph on a stream the call creates (the caller's stream
  * may be the legacy null stream); with kernel-class profiling on, all run directly. The call
  * returns after the device finished; the caller's stream is ordered after the work. It allocates
- * only that stream, one event and the graph, and releases them before returning.
+ * only that stream, one event and the graph, and releases them before returning. With `kv` the
+ * loop runs over the tokens after a cached prefix (the prefix-KV decode mode): every iteration
+ * reads the cache, none writes it (dcl_kv_append does).
  * 1 <= max_steps, 1 <= check_every; other argument rules as for the two calls. */
 dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S, int32_t* p,
                         int32_t gen_end, const dcl_kv* kv, uint32_t score_flags, int32_t L,
