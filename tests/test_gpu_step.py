@@ -271,15 +271,18 @@ def test_entropy_of_steered_and_flat_rows():
     assert abs(st["entropy"][0] - H[0]) < 2 * LOGIT_TOL
 
 
-def test_kv_prefix_step_ragged_gqa_with_spare_capacity():
-    """A 40-key prefix (a 64-key tile then holds cache and fresh keys), 21 fresh tokens (S not a
-    multiple of 8), GQA 4/2 with head_dim 128 and q/k/v bias, and a cache whose capacity (48)
-    exceeds the prefix: the unused positions hold large finite values that must never be read."""
+@pytest.mark.parametrize("key,B,P,S,cap", [("gqa_bias_dh128", 3, 40, 21, 48), ("dream_2l", 2, 72, 27, 80)])
+def test_kv_prefix_step_ragged_gqa_with_spare_capacity(key, B, P, S, cap):
+    """A prefix that is not a multiple of 64 keys (a 64-key tile then holds cache and fresh keys),
+    fresh tokens not a multiple of 8, GQA with head_dim 128 and q/k/v bias (a small model, and two
+    layers of the Dream-7B geometry: 28/4 heads, d 3584, vocabulary 152064), and a cache whose
+    capacity exceeds the prefix: the unused positions hold large finite values that must never be
+    read."""
     import torch
-    base = CASES["gqa_bias_dh128"]
-    w = dataclasses.replace(base, key="kv_ragged", batch=3, prompt_len=0, gen_len=21, window=8, p=0, draft=(8, 16),
-                            kv_prefix=40, kv_seed=5)
-    stored = _setup("gqa_bias_dh128")[1]
+    base = CASES[key]
+    w = dataclasses.replace(base, key="kv_ragged_" + key, batch=B, prompt_len=0, gen_len=S, window=8, p=0,
+                            draft=(8, 16), kv_prefix=P, kv_seed=5)
+    stored = _setup(key)[1]
     W = WeightView(stored)
     run = runner_for(w, stored)
     g = w.geom
@@ -292,7 +295,6 @@ def test_kv_prefix_step_ragged_gqa_with_spare_capacity():
     tok, p = synth.initial_state(w)
     ref = oracle.step(g, W, tok, p, w.gen_end, kv=kv)
     ct, lt = derived_tolerance(g, W, tok, p, w.gen_end, ref, kv=kv)
-    cap, P = 48, w.kv_prefix
     big = np.uint16(0x4700)                          # bf16 32768
     ks, vs = [], []
     for k, v in caches:
