@@ -44,3 +44,17 @@ def test_more_than_one_gpu_is_refused():
                        timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_stored_traffic_follows_the_kernel_source_digest(monkeypatch):
+    """The committed counter traffic is reported only while the GEMM sources it was measured on are
+    unchanged: a different digest drops it (the roofline then reports traffic as null)."""
+    rec = bench.stored_traffic("gemm_gate_up_swiglu", "c2")
+    if rec is not None:
+        assert rec["source_digest"] == bench.kernel_source_digest()
+        assert rec["hbm_bytes_per_launch"] == rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+        assert rec["algorithmic_bytes_per_launch"] == \
+            bench.step_bytes(synth.WORKLOADS["c2"], 256)["gemm_gate_up_swiglu"]
+    monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 16)
+    assert bench.stored_traffic("gemm_gate_up_swiglu", "c2") is None
+    assert bench.stored_traffic("no_such_class", "c2") is None
