@@ -19,6 +19,10 @@ The residual stream r is never rounded.
 ``dtype=np.float32`` evaluates the same definition in float32 arithmetic. It is not the
 reference; it measures how far any float32 implementation of this rounding list lands from the
 float64 result, which sizes the whole-step tolerance of the GPU parity tests.
+
+The stage functions (``norm_stage``, ``qkv_stage``, ``attention_stage``, ``swiglu_stage``,
+``residual_stage``) are the steps of one layer in the order above; ``forward`` composes them, and the
+stage-wise parity tests call them one at a time on given stage inputs.
 """
 from typing import Callable, Mapping, Optional, Tuple
 
@@ -30,6 +34,69 @@ from .numerics import apply_rope, bf16_round, rmsnorm, rope_tables, silu
 def _w(weights, name, dtype=np.float64) -> Optional[np.ndarray]:
     v = weights[name] if not callable(weights) else weights(name)
     return None if v is None else np.asarray(v, dtype=dtype)
+
+
+def norm_stage(r, gain, eps, rnd):
+    """u = bf16(rmsnorm(r) * g): the normalised operand of the next projection."""
+    return rnd(rmsnorm(r, gain, eps))
+
+
+def qkv_stage(geom, W, l, u, cos, sin, rnd, rope=True):
+    """q, k, v of layer ``l`` for the rows of ``u`` [S, d]: projections (+ bias), rotate-half RoPE on
+    q and k at the positions of ``cos``/``sin`` [S, dh/2], then the bf16 storage point.
+    Returns q [H, S, dh], k [Hkv, S, dh], v [Hkv, S, dh]."""
+    H, Hkv, dh = geom.n_heads, geom.n_kv_heads, geom.head_dim
+    S = u.shape[0]
+    p = f"l{l}."
+    q = u @ W(p + "wq").T
+    k = u @ W(p + "wk").T
+    v = u @ W(p + "wv").T
+    if geom.qkv_bias:
+        q = q + W(p + "bq")
+        k = k + W(p + "bk")
+        v = v + W(p + "bv")
+    q = q.reshape(S, H, dh).transpose(1, 0, 2)
+    k = k.reshape(S, Hkv, dh).transpose(1, 0, 2)
+    v = v.reshape(S, Hkv, dh).transpose(1, 0, 2)
+    if rope:
+        q = apply_rope(q, cos, sin)
+        k = apply_rope(k, cos, sin)
+    return rnd(q), rnd(k), rnd(v)
+
+
+def attention_stage(geom, q, k, v, rnd, dtype=np.float64):
+    """o = bf16(softmax(q k^T / sqrt(dh)) v) per head over ALL keys (no mask), query head h reading
+    key/value head h // (H / Hkv). q [H, Sq, dh], k and v [Hkv, Sk, dh]; returns o [Sq, H*dh]."""
+    H, Hkv, dh = geom.n_heads, geom.n_kv_heads, geom.head_dim
+    group = H // Hkv
+    Sq = q.shape[1]
+    o = np.empty((H, Sq, dh), np.dtype(dtype))
+    for h in range(H):
+        g = h // group
+        s = (q[h] @ k[g].T) / float(np.sqrt(dh))
+        s = np.exp(s - s.max(axis=1, keepdims=True))
+        P = s / s.sum(axis=1, keepdims=True)
+        o[h] = P @ v[g]
+    return rnd(o.transpose(1, 0, 2).reshape(Sq, H * dh))
+
+
+def swiglu_stage(W, l, u2, rnd):
+    """a = bf16(silu(u2 Wg^T) * (u2 Wu^T))."""
+    p = f"l{l}."
+    return rnd(silu(u2 @ W(p + "wg").T) * (u2 @ W(p + "wu").T))
+
+
+def residual_stage(r, x, w):
+    """r + x w^T (the residual stream is never rounded)."""
+    return r + x @ w.T
+
+
+def rounding(bf16_boundary, dtype=np.float64):
+    """The storage-point rounding of the chosen mode: bf16 (then widened to ``dtype``) or none."""
+    dt = np.dtype(dtype)
+    if bf16_boundary:
+        return lambda a: bf16_round(a).astype(dt)
+    return lambda a: a
 
 
 def forward(geom, weights, tokens: np.ndarray, positions: np.ndarray,
@@ -44,18 +111,13 @@ def forward(geom, weights, tokens: np.ndarray, positions: np.ndarray,
     kv: optional callable layer -> (Kc [Hkv, P, dh], Vc [Hkv, dh, P]) cached prefix
         (keys already rotated); the S fresh tokens then attend to [cache || fresh].
     rope: False disables the rotary embedding (used by the permutation pin).
+    return_residuals: also return the residual stream before layer 0 and after every layer.
     return_kv: also return the per-layer (k [Hkv,S,dh], v [Hkv,dh,S]) of the S tokens, as a cache would
         hold them.
     """
     dt = np.dtype(dtype)
-    if bf16_boundary:
-        rnd = lambda a: bf16_round(a).astype(dt)
-    else:
-        rnd = lambda a: a
-    d, H, Hkv, dh = geom.d_model, geom.n_heads, geom.n_kv_heads, geom.head_dim
-    S = len(tokens)
-    group = H // Hkv
-    cos, sin = (t.astype(dt) for t in rope_tables(positions, dh, geom.rope_base))
+    rnd = rounding(bf16_boundary, dt)
+    cos, sin = (t.astype(dt) for t in rope_tables(positions, geom.head_dim, geom.rope_base))
     W = lambda name: _w(weights, name, dt)
 
     r = W("embed")[np.asarray(tokens)]                           # [S, d]
@@ -63,42 +125,22 @@ def forward(geom, weights, tokens: np.ndarray, positions: np.ndarray,
     kv_out = [] if return_kv else None
     for l in range(geom.n_layers):
         p = f"l{l}."
-        u = rnd(rmsnorm(r, W(p + "g1"), geom.rms_eps))
-        q = u @ W(p + "wq").T
-        k = u @ W(p + "wk").T
-        v = u @ W(p + "wv").T
-        if geom.qkv_bias:
-            q = q + W(p + "bq")
-            k = k + W(p + "bk")
-            v = v + W(p + "bv")
-        q = q.reshape(S, H, dh).transpose(1, 0, 2)                # [H, S, dh]
-        k = k.reshape(S, Hkv, dh).transpose(1, 0, 2)              # [Hkv, S, dh]
-        v = v.reshape(S, Hkv, dh).transpose(1, 0, 2)
-        if rope:
-            q = apply_rope(q, cos, sin)
-            k = apply_rope(k, cos, sin)
-        q, k, v = rnd(q), rnd(k), rnd(v)
+        u = norm_stage(r, W(p + "g1"), geom.rms_eps, rnd)
+        q, k, v = qkv_stage(geom, W, l, u, cos, sin, rnd, rope)
         if return_kv:
             kv_out.append((k.copy(), v.transpose(0, 2, 1).copy()))
         if kv is not None:
             kc, vc = kv(l)
             k = np.concatenate([np.asarray(kc, dt), k], axis=1)
             v = np.concatenate([np.asarray(vc, dt).transpose(0, 2, 1), v], axis=1)
-        o = np.empty((H, S, dh), dt)
-        for h in range(H):
-            g = h // group
-            s = (q[h] @ k[g].T) / float(np.sqrt(dh))                     # [S, Sk], no mask
-            s = np.exp(s - s.max(axis=1, keepdims=True))
-            P = s / s.sum(axis=1, keepdims=True)
-            o[h] = P @ v[g]
-        o = rnd(o.transpose(1, 0, 2).reshape(S, H * dh))
-        r = r + o @ W(p + "wo").T
-        u2 = rnd(rmsnorm(r, W(p + "g2"), geom.rms_eps))
-        a = rnd(silu(u2 @ W(p + "wg").T) * (u2 @ W(p + "wu").T))
-        r = r + a @ W(p + "wd").T
+        o = attention_stage(geom, q, k, v, rnd, dt)
+        r = residual_stage(r, o, W(p + "wo"))
+        u2 = norm_stage(r, W(p + "g2"), geom.rms_eps, rnd)
+        a = swiglu_stage(W, l, u2, rnd)
+        r = residual_stage(r, a, W(p + "wd"))
         if return_residuals:
             residuals.append(r.copy())
-    hf = rnd(rmsnorm(r, W("gf"), geom.rms_eps))
+    hf = norm_stage(r, W("gf"), geom.rms_eps, rnd)
     extra = ([residuals] if return_residuals else []) + ([kv_out] if return_kv else [])
     return (hf, *extra) if extra else hf
 

@@ -22,10 +22,16 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
 
 
 def rmsnorm(r: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:
-    """r / sqrt(mean(r^2) + eps) * gain over the last axis."""
-    r = np.asarray(r, dtype=np.float64)
-    inv = 1.0 / np.sqrt(np.mean(r * r, axis=-1, keepdims=True) + eps)
-    return (r * inv) * np.asarray(gain, dtype=np.float64)
+    """r / sqrt(mean(r^2) + eps) * gain over the last axis.
+
+    Evaluated in float32 when ``r`` is float32 (the float32 evaluation of the whole definition,
+    used only to size tolerances), in float64 otherwise."""
+    r = np.asarray(r)
+    dt = np.float32 if r.dtype == np.float32 else np.float64
+    r = r.astype(dt, copy=False)
+    ms = np.mean(r * r, axis=-1, keepdims=True, dtype=dt)
+    inv = dt(1.0) / np.sqrt(ms + dt(eps))
+    return (r * inv) * np.asarray(gain, dtype=dt)
 
 
 def rope_tables(positions: np.ndarray, head_dim: int, base: float):

@@ -9,6 +9,9 @@ Readings of the paper used here (the paper is silent or inconsistent on them):
 * K = 0 would stall Algorithm 1, so by default K_eff = max(K, 1) (the top-1 at p
   is committed, i.e. one sequential chain-rule step, Section 2.2); the
   ``no_progress_guard`` flag keeps the literal K;
+* a window start whose row carries no statistics (top1 = -1: the row was not scored, which only
+  happens when the caller did not re-mask the window) has no prediction to commit: K_eff stays 0
+  and the sequence does not advance in that iteration;
 * scored rows (``score_all=False``): x_i = [MASK] and p <= i < gen_end (probabilities
   are defined at masked positions, Section 2.1); only those rows can become drafts.
   ``score_all=True``: every position p <= i < gen_end is scored and may be redrafted.
@@ -42,7 +45,7 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
     Returns (new tokens, new p, K_raw [B], K_eff [B]); inputs are not modified.
     Per sequence with p < gen_end:
       L_eff = min(L, gen_end - p); K = Eq. compute_k over conf[p : p + L_eff];
-      K_eff = max(K, 1) (unless no_progress_guard);
+      K_eff = max(K, 1) (unless no_progress_guard, or the row at p has no prediction: top1 = -1);
       commit x[p : p + K_eff] = top1                                 (Algorithm 1, commit)
       for j in [p + L, gen_end): if (x_j = [MASK] or score_all) and conf_j > tau_draft:
           x_j = top1_j                                               (Eq. draft_update)
@@ -63,7 +66,8 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
             continue
         L_eff = min(L, gen_end - pb)
         K = compute_k(conf[b, pb:pb + L_eff], tau_commit)
-        Ke = K if no_progress_guard else max(K, 1)
+        has_prediction = top1[b, pb] >= 0
+        Ke = K if (no_progress_guard or not has_prediction) else max(K, 1)
         K_raw[b], K_eff[b] = K, Ke
         for j in range(pb, pb + Ke):
             x[b, j] = top1[b, j]

@@ -50,6 +50,10 @@ def run(key, stored):
     rows = np.nonzero(m.reshape(-1))[0]
     x, pn, kr, ke = oracle.select_contiguous(tok, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id,
                                              ref["top1"], ref["conf"])
+    # the same selection on the float32 evaluation's statistics: how often a float32 implementation of the
+    # definition alone already lands on another K
+    _, _, kr32, _ = oracle.select_contiguous(tok, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id,
+                                             f32["top1"], f32["conf"].astype(np.float64))
     out = dict(tokens=tok, p=p, rows=rows.astype(np.int64),
                top1=ref["top1"].reshape(-1)[rows], top2=ref["top2"].reshape(-1)[rows],
                conf=ref["conf"].reshape(-1)[rows], p2=ref["p2"].reshape(-1)[rows], lse=ref["lse"].reshape(-1)[rows],
@@ -58,12 +62,13 @@ def run(key, stored):
                f32_top1_flips=np.int64((f32["top1"][m] != ref["top1"][m]).sum()),
                f32_conf=f32["conf"].reshape(-1)[rows], f32_lse=f32["lse"].reshape(-1)[rows],
                f32_top1=f32["top1"].reshape(-1)[rows],
-               sel_tokens=x, sel_p=pn, sel_k_raw=kr, sel_k_eff=ke,
+               sel_tokens=x, sel_p=pn, sel_k_raw=kr, sel_k_eff=ke, f32_sel_k_raw=kr32,
                checksum_names=np.array(CHECK_TENSORS), checksum_values=np.array([checksums(stored)[n] for n in CHECK_TENSORS]),
                oracle_seconds=np.float64(t1 - t0))
     np.savez_compressed(os.path.join(HERE, f"full_{key}.npz"), **out)
     print(f"{key}: {len(rows)} scored rows, oracle {t1 - t0:.0f} s, float32 evaluation {t2 - t1:.0f} s, "
-          f"drift conf {out['drift_conf']:.3g} lse {out['drift_lse']:.3g}, K_eff {ke.tolist()}", flush=True)
+          f"drift conf {out['drift_conf']:.3g} lse {out['drift_lse']:.3g}, K_eff {ke.tolist()}, "
+          f"K of the float32 evaluation {kr32.tolist()}", flush=True)
 
 
 def main(keys):

@@ -4,6 +4,8 @@ The paper prints no numbers for the forward, so these pins are library routines
 (torch.nn.functional in float64, numpy complex arithmetic), textbook identities
 and invariants.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -76,7 +78,7 @@ def test_rope_identity_norm_and_relative_position():
     np.testing.assert_allclose(dots, dots[0], rtol=1e-9)
 
 
-def _torch_forward(geom, W, tokens, positions, bf16_boundary=True):
+def _torch_forward(geom, W, tokens, positions, bf16_boundary=True, bias_after_rope=False):
     """Second opinion from torch.nn.functional (float64): rms_norm, complex RoPE, SDPA, silu."""
     t = lambda n: torch.from_numpy(np.asarray(W(n), np.float64))
     d, H, Hkv, dh = geom.d_model, geom.n_heads, geom.n_kv_heads, geom.head_dim
@@ -97,10 +99,18 @@ def _torch_forward(geom, W, tokens, positions, bf16_boundary=True):
     for l in range(geom.n_layers):
         p = f"l{l}."
         u = rnd(F.rms_norm(r, (d,), t(p + "g1"), eps=geom.rms_eps))
-        q = (u @ t(p + "wq").T).view(S, H, dh).transpose(0, 1)
-        k = (u @ t(p + "wk").T).view(S, Hkv, dh).transpose(0, 1)
-        v = (u @ t(p + "wv").T).view(S, Hkv, dh).transpose(0, 1)
-        q, k, v = rnd(rope(q)), rnd(rope(k)), rnd(v)
+        # nn.Linear with bias (Qwen2.5 / Dream geometry), before the rotation; bias_after_rope is the
+        # plausible mistake the pin must reject
+        bias = (lambda n: t(p + n)) if geom.qkv_bias and not bias_after_rope else (lambda n: None)
+        q = F.linear(u, t(p + "wq"), bias("bq")).view(S, H, dh).transpose(0, 1)
+        k = F.linear(u, t(p + "wk"), bias("bk")).view(S, Hkv, dh).transpose(0, 1)
+        v = F.linear(u, t(p + "wv"), bias("bv")).view(S, Hkv, dh).transpose(0, 1)
+        q, k = rope(q), rope(k)
+        if geom.qkv_bias and bias_after_rope:
+            q = q + t(p + "bq").view(H, 1, dh)
+            k = k + t(p + "bk").view(Hkv, 1, dh)
+            v = v + t(p + "bv").view(Hkv, 1, dh)
+        q, k, v = rnd(q), rnd(k), rnd(v)
         k = k.repeat_interleave(H // Hkv, 0)
         v = v.repeat_interleave(H // Hkv, 0)
         o = F.scaled_dot_product_attention(q[None], k[None], v[None], is_causal=False)[0]
@@ -112,10 +122,26 @@ def _torch_forward(geom, W, tokens, positions, bf16_boundary=True):
     return rnd(F.rms_norm(r, (d,), t("gf"), eps=geom.rms_eps)).numpy()
 
 
-@pytest.mark.parametrize("key", ["c1", "c1s"])
+# Dream-style geometry at test size: head_dim 128, GQA 4/2, q/k/v biases, RoPE base 1e6, eps 1e-6
+GQA_BIAS = dataclasses.replace(
+    synth.WORKLOADS["c1s"], key="gqa_bias_dh128", batch=1,
+    geom=dataclasses.replace(synth.WORKLOADS["c1s"].geom, name="gqa_bias_dh128", n_heads=4, n_kv_heads=2,
+                             head_dim=128, d_model=384, d_ffn=768, qkv_bias=True, weight_dtype="bf16",
+                             rope_base=1e6, rms_eps=1e-6))
+
+
+def _case(tiny_weights, key):
+    if key != "gqa_bias_dh128":
+        w, stored, _ = tiny_weights(key)
+        return w, stored
+    return GQA_BIAS, synth.make_weights(GQA_BIAS.geom)
+
+
+@pytest.mark.parametrize("key", ["c1", "c1s", "gqa_bias_dh128"])
 def test_forward_matches_torch_functional_pure(tiny_weights, key):
-    """Without the bf16 storage roundings both float64 forwards agree to rounding noise."""
-    w, stored, _ = tiny_weights(key)
+    """Without the bf16 storage roundings both float64 forwards agree to rounding noise (with q/k/v
+    biases and GQA on the Dream-style geometry)."""
+    w, stored = _case(tiny_weights, key)
     W = WeightView(stored, bf16_boundary=False)
     tok, p = synth.initial_state(w)
     pos = np.arange(w.seq)
@@ -124,11 +150,12 @@ def test_forward_matches_torch_functional_pure(tiny_weights, key):
     np.testing.assert_allclose(ours, ref, rtol=1e-10, atol=1e-10)
 
 
-@pytest.mark.parametrize("key", ["c1", "c1s"])
+@pytest.mark.parametrize("key", ["c1", "c1s", "gqa_bias_dh128"])
 def test_forward_matches_torch_functional_bf16(tiny_weights, key):
     """With the storage roundings, an occasional one-ulp flip propagates; rows still agree to a few
     bf16 ulps of their scale."""
-    w, stored, W = tiny_weights(key)
+    w, stored = _case(tiny_weights, key)
+    W = WeightView(stored)
     tok, p = synth.initial_state(w)
     pos = np.arange(w.seq)
     ours = oracle.forward(w.geom, W, tok[0], pos)
@@ -207,3 +234,47 @@ def test_coordinate_permutation_is_a_symmetry(tiny_weights):
     s1 = oracle.step(w.geom, permuted_weights(W, w.geom, 5), tok, p, w.gen_end)
     np.testing.assert_array_equal(s0["top1"], s1["top1"])
     np.testing.assert_allclose(s0["conf"], s1["conf"], rtol=1e-9, atol=1e-12)
+
+
+def test_bias_enters_before_the_rotation():
+    """The q/k biases belong to the projection that RoPE rotates. The torch opinion with the biases added
+    after the rotation is a different function, far outside the 1e-10 agreement of the pure-mode pin,
+    so that pin rejects the wrong order."""
+    w = GQA_BIAS
+    stored = synth.make_weights(w.geom)
+    W = WeightView(stored, bf16_boundary=False)
+    tok, _ = synth.initial_state(w)
+    pos = np.arange(w.seq)
+    ours = oracle.forward(w.geom, W, tok[0], pos, bf16_boundary=False)
+    wrong = _torch_forward(w.geom, W, tok[0], pos, bf16_boundary=False, bias_after_rope=True)
+    assert np.abs(ours - wrong).max() > 1e-3
+
+
+def test_lm_logits_chunking_equals_one_product():
+    """lm_logits walks the vocabulary in chunks; with V larger than the chunk (and a ragged last chunk)
+    it equals one unchunked product h_f W^T."""
+    rng = np.random.default_rng(11)
+    V, d = 20011, 64
+    Wl = rng.standard_normal((V, d))
+    hf = rng.standard_normal((9, d))
+    ref = hf @ Wl.T
+    for chunk in (8192, 7, V, 3 * V):
+        np.testing.assert_allclose(oracle.lm_logits({"lm_head": Wl}, hf, chunk=chunk), ref, rtol=1e-12, atol=1e-12)
+    # through the lazy bf16 weight view (uint16 bit patterns widened exactly)
+    bits = synth.normal_bf16(5, 0, 0.5, (V, d))
+    view = WeightView({"lm_head": bits})
+    np.testing.assert_allclose(oracle.lm_logits(view, hf), hf @ synth.bf16_bits_to_f32(bits).astype(np.float64).T,
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_float32_evaluation_runs_in_float32():
+    """The float32 evaluation that sizes tolerances must keep float32 arithmetic end to end, RMSNorm
+    included: its RMSNorm differs from the float64 one by float32 rounding, not by zero."""
+    rng = np.random.default_rng(12)
+    r = (rng.standard_normal((64, 512)) * 3).astype(np.float32)
+    g = np.ones(512, np.float32)
+    a = rmsnorm(r, g, 1e-5)
+    assert a.dtype == np.float32
+    b = rmsnorm(r.astype(np.float64), g, 1e-5)
+    d = np.abs(a - b).max()
+    assert 0 < d < 1e-5 * np.abs(b).max()

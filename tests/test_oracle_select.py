@@ -113,7 +113,10 @@ def test_select_rules_per_position():
             pb = p[b]
             Le = min(L, end - pb)
             first_fail = next((j for j in range(Le) if not conf[b, pb + j] > tc), Le)
-            assert kr[b] == first_fail and ke[b] == max(first_fail, 1) and pn[b] == pb + ke[b]
+            # reading R18: an unscored window start (no prediction at p) commits nothing
+            want_ke = max(first_fail, 1) if top1[b, pb] >= 0 else first_fail
+            assert kr[b] == first_fail and ke[b] == want_ke and pn[b] == pb + ke[b]
+            assert (x[b] >= 0).all()                                                     # no sentinel committed
             np.testing.assert_array_equal(x[b, :pb], tok[b, :pb])                       # history immutable
             np.testing.assert_array_equal(x[b, pb:pn[b]], top1[b, pb:pn[b]])             # commit
             np.testing.assert_array_equal(x[b, pn[b]:min(pn[b] + L, end)], mask)         # remask
