@@ -238,6 +238,37 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
                             const dcl_kv* kv, const int32_t* rows, int32_t n_rows, float* out,
                             void* hidden_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Test support: the intermediate tensors of one transformer layer, each a device buffer of the stated
+ * layout or NULL (not written). T = B*S, Sp = S rounded up to a multiple of 8. */
+typedef struct {
+  void* u;       /* bf16 [T, d_model]: bf16(RMSNorm(r_in) * g_attn) */
+  void* q;       /* bf16 [B, n_heads, S, head_dim]: queries after bias and RoPE */
+  void* k;       /* bf16 [B, n_kv_heads, S, head_dim]: keys after bias and RoPE */
+  void* v;       /* bf16 [B, n_kv_heads, head_dim, Sp]: values, key index contiguous (keys >= S are 0) */
+  void* o;       /* bf16 [T, n_heads * head_dim]: attention output (softmax(q k^T / sqrt(dh)) v, no mask) */
+  float* r_mid;  /* [T, d_model]: r_in + o W_o^T */
+  void* u2;      /* bf16 [T, d_model]: bf16(RMSNorm(r_mid) * g_ffn) */
+  void* a;       /* bf16 [T, d_ffn]: bf16(silu(u2 W_gate^T) * (u2 W_up^T)) */
+  float* r_out;  /* [T, d_model]: r_mid + a W_down^T, the next layer's input */
+} dcl_layer_taps;
+
+/* Test support: layer `layer` of the forward of dcl_denoise_step (Algorithm 1, Forward) run alone on the
+ * float32 residual stream r_in (device [B*S, d_model], the layer's input), with the same kernels, tile
+ * plans and split-K folding as a step over B sequences of S tokens (tokens at positions
+ * kv->prefix_len + i, attending to the cached prefix when kv != NULL). Every non-NULL tap receives
+ * that intermediate; chaining r_out into the next call from the embedding rows reproduces the step's
+ * residual stream bit for bit. ws as for dcl_denoise_step (its contents are overwritten). */
+dcl_status dcl_debug_layer(dcl_model_t model, int32_t B, int32_t S, const dcl_kv* kv, int32_t layer,
+                           const float* r_in, dcl_layer_taps taps, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Test support (host only): the tile plan a GEMM of Nw weight rows, T tokens and depth K runs with.
+ * lm_head = 1 asks for the fused LM-head plan (vocabulary tiles of 128 ids), otherwise the plan of a
+ * residual GEMM allowed max_split (1..4) K-split slices. info (host int32[8]) receives
+ * {configuration index, K-split slices, weight rows, tokens, K depth per stage, stages, waves along
+ * the weight rows, waves along the tokens}; an LM-head plan whose weight rows per wave equal 128 has
+ * every wave own a whole vocabulary tile. */
+dcl_status dcl_debug_gemm_plan(int32_t Nw, int32_t T, int32_t K, int32_t lm_head, int32_t max_split, int32_t* info);
+
 /* Kernel-class timing (profiling support for benchmarks). While enabled, every kernel launch
  * made by dcl_denoise_step / dcl_score_hidden / dcl_select_contiguous is bracketed by a pair of
  * hipEvents recorded on the caller's stream (this adds a little host work per launch; leave it

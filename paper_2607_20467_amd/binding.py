@@ -3,6 +3,12 @@
 Device buffers are torch tensors on ``cuda`` (ROCm); their ``data_ptr()`` and the current
 stream's handle are passed through unchanged. Every step of the computation runs in the
 library's HIP kernels.
+
+Before a call, every tensor argument is checked against what the call will read or write
+through it: on the device, contiguous, of the element type the C declaration states (int32
+ids and positions, float32 statistics and residuals, 16-bit bfloat16 patterns), and holding at
+least the elements the sizes imply. A failed check raises ``DclError`` (DCL_E_ARG) before the
+library is called. Plain integers are taken as raw device addresses and passed unchecked.
 """
 import ctypes
 import os
@@ -47,6 +53,10 @@ class DclProfile(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int64 * len(PROF_CLASSES)), ("ms", ctypes.c_double * len(PROF_CLASSES))]
 
 
+class DclLayerTaps(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("u", "q", "k", "v", "o", "r_mid", "u2", "a", "r_out")]
+
+
 class DclKV(ctypes.Structure):
     _fields_ = [("k", ctypes.POINTER(ctypes.c_void_p)), ("v", ctypes.POINTER(ctypes.c_void_p)),
                 ("prefix_len", ctypes.c_int32), ("capacity", ctypes.c_int32)]
@@ -89,6 +99,8 @@ def load_library():
         "dcl_profile_read": (ctypes.c_int, [ctypes.POINTER(DclProfile)]),
         "dcl_score_hidden": (ctypes.c_int, [vp, vp, i32, DclRowStats, vp, sz, vp]),
         "dcl_debug_logits": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, i32, vp, vp, vp, sz, vp]),
+        "dcl_debug_layer": (ctypes.c_int, [vp, i32, i32, ctypes.POINTER(DclKV), i32, vp, DclLayerTaps, vp, sz, vp]),
+        "dcl_debug_gemm_plan": (ctypes.c_int, [i32, i32, i32, i32, i32, ctypes.POINTER(i32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -111,6 +123,42 @@ def _ptr(x) -> Optional[int]:
     return x.data_ptr()
 
 
+_I32 = ("int32",)
+_F32 = ("float32",)
+_B16 = ("int16", "bfloat16", "uint16")       # bfloat16 bit patterns
+_ANY = None
+
+
+def _arg(x, name, where, kinds, numel=None, nbytes=None):
+    """Device address of tensor argument ``x`` after checking it against the call: device memory,
+    contiguous, element type among ``kinds`` (torch dtype names; None = any), at least ``numel``
+    elements and ``nbytes`` bytes. None stays None; an int is a raw address and is not checked."""
+    if x is None or isinstance(x, int):
+        return x
+    bad = None
+    if not getattr(x, "is_cuda", False):
+        bad = "must be a device (cuda) tensor"
+    elif not x.is_contiguous():
+        bad = "must be contiguous"
+    elif kinds is not None and str(x.dtype).replace("torch.", "") not in kinds:
+        bad = f"has dtype {x.dtype}, expected {' or '.join(kinds)}"
+    elif numel is not None and x.numel() < numel:
+        bad = f"holds {x.numel()} elements, the call needs {numel}"
+    elif nbytes is not None and x.numel() * x.element_size() < nbytes:
+        bad = f"holds {x.numel() * x.element_size()} bytes, the call needs {nbytes}"
+    if bad:
+        raise DclError(1, where, f"{name} {bad}")
+    return x.data_ptr()
+
+
+# Geometry of every handle this binding created (sizes for the argument checks).
+_geometry = {}
+
+
+def _cfg_of(model):
+    return _geometry.get(model)
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         import torch
@@ -131,10 +179,12 @@ def dcl_last_error() -> str:
 def dcl_model_create(cfg: DclConfig) -> int:
     h = ctypes.c_void_p()
     _check(load_library().dcl_model_create(ctypes.byref(cfg), ctypes.byref(h)), "dcl_model_create")
+    _geometry[h.value] = DclConfig.from_buffer_copy(cfg)
     return h.value
 
 
 def dcl_model_destroy(model: int) -> None:
+    _geometry.pop(model, None)
     load_library().dcl_model_destroy(model)
 
 
@@ -145,7 +195,8 @@ def dcl_weights_bytes(cfg: DclConfig) -> int:
 def dcl_load_weights(model: int, dev_buf, nbytes: int, src_ptrs: Sequence[Optional[int]], src_dtype: int,
                      stream=None) -> None:
     arr = (ctypes.c_void_p * len(src_ptrs))(*src_ptrs)
-    _check(load_library().dcl_load_weights(model, _ptr(dev_buf), nbytes, arr, len(src_ptrs), src_dtype,
+    buf = _arg(dev_buf, "dev_buf", "dcl_load_weights", _ANY, nbytes=nbytes)
+    _check(load_library().dcl_load_weights(model, buf, nbytes, arr, len(src_ptrs), src_dtype,
                                            _stream(stream)), "dcl_load_weights")
 
 
@@ -153,57 +204,78 @@ def dcl_workspace_bytes(model: int, B: int, S: int, kv_prefix: int = 0) -> int:
     return load_library().dcl_workspace_bytes(model, B, S, kv_prefix)
 
 
-def _stats(st) -> DclRowStats:
-    """st: dict of device arrays; "entropy" is optional (not written when absent)."""
-    return DclRowStats(*(_ptr(st.get(k)) for k in ("top1", "top2", "conf", "p2", "lse", "entropy")))
+def _stats(st, n=None, where="") -> DclRowStats:
+    """st: dict of device arrays (each >= n elements); "entropy" is optional (not written when absent)."""
+    kinds = {"top1": _I32, "top2": _I32, "conf": _F32, "p2": _F32, "lse": _F32, "entropy": _F32}
+    return DclRowStats(*(_arg(st.get(k), f"stats[{k!r}]", where, kinds[k], n) for k in kinds))
 
 
-def _kv(kv):
+def _kv(kv, model=None, B=None, where=""):
     """kv: None or (per-layer K tensors, per-layer V tensors, prefix_len[, capacity])."""
     if kv is None:
         return None, None
     ks, vs, P = kv[:3]
     cap = kv[3] if len(kv) > 3 else 0
-    ka = (ctypes.c_void_p * len(ks))(*[_ptr(t) for t in ks])
-    va = (ctypes.c_void_p * len(vs))(*[_ptr(t) for t in vs])
+    g = _cfg_of(model)
+    need = None
+    if g is not None and B is not None:
+        if len(ks) != g.n_layers or len(vs) != g.n_layers:
+            raise DclError(1, where, f"kv holds {len(ks)}/{len(vs)} layers, the model has {g.n_layers}")
+        need = B * g.n_kv_heads * (cap or P) * g.head_dim
+    ka = (ctypes.c_void_p * len(ks))(*[_arg(t, f"kv K[{i}]", where, _B16, need) for i, t in enumerate(ks)])
+    va = (ctypes.c_void_p * len(vs))(*[_arg(t, f"kv V[{i}]", where, _B16, need) for i, t in enumerate(vs)])
     s = DclKV(ctypes.cast(ka, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(va, ctypes.POINTER(ctypes.c_void_p)), P,
               cap)
     return ctypes.byref(s), (s, ka, va)
 
 
+def _state(tokens, p, B, S, where):
+    n = B * S if B > 0 and S > 0 else None
+    return (_arg(tokens, "tokens", where, _I32, n), _arg(p, "p", where, _I32, B if B > 0 else None))
+
+
 def dcl_denoise_step(model: int, tokens, B: int, S: int, p, gen_end: int, kv, flags: int, stats, ws, ws_bytes: int,
                      stream=None) -> None:
-    kvp, keep = _kv(kv)
-    _check(load_library().dcl_denoise_step(model, _ptr(tokens), B, S, _ptr(p), gen_end, kvp, flags, _stats(stats),
-                                           _ptr(ws), ws_bytes, _stream(stream)), "dcl_denoise_step")
+    w = "dcl_denoise_step"
+    kvp, keep = _kv(kv, model, B, w)
+    tp, pp = _state(tokens, p, B, S, w)
+    _check(load_library().dcl_denoise_step(model, tp, B, S, pp, gen_end, kvp, flags, _stats(stats, B * S, w),
+                                           _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes, _stream(stream)), w)
     del keep
 
 
 def dcl_select_contiguous(tokens, B: int, S: int, p, gen_end: int, L: int, tau_commit: float, tau_draft: float,
                           mask_id: int, stats, k_raw=None, k_eff=None, flags: int = 0, stream=None) -> None:
-    _check(load_library().dcl_select_contiguous(_ptr(tokens), B, S, _ptr(p), gen_end, L, tau_commit, tau_draft,
-                                                mask_id, _stats(stats), _ptr(k_raw), _ptr(k_eff), flags,
-                                                _stream(stream)), "dcl_select_contiguous")
+    w = "dcl_select_contiguous"
+    tp, pp = _state(tokens, p, B, S, w)
+    _check(load_library().dcl_select_contiguous(tp, B, S, pp, gen_end, L, tau_commit, tau_draft, mask_id,
+                                                _stats(stats, B * S, w), _arg(k_raw, "k_raw", w, _I32, B),
+                                                _arg(k_eff, "k_eff", w, _I32, B), flags, _stream(stream)), w)
 
 
 def dcl_generate(model: int, tokens, B: int, S: int, p, gen_end: int, kv, score_flags: int, L: int,
                  tau_commit: float, tau_draft: float, select_flags: int, max_steps: int, check_every: int, stats,
                  k_raw, k_eff, k_hist, ws, ws_bytes: int, stream=None) -> int:
     """Returns the number of iterations run."""
-    kvp, keep = _kv(kv)
+    w = "dcl_generate"
+    kvp, keep = _kv(kv, model, B, w)
+    tp, pp = _state(tokens, p, B, S, w)
     steps = ctypes.c_int32(0)
-    _check(load_library().dcl_generate(model, _ptr(tokens), B, S, _ptr(p), gen_end, kvp, score_flags, L, tau_commit,
-                                       tau_draft, select_flags, max_steps, check_every, _stats(stats), _ptr(k_raw),
-                                       _ptr(k_eff), _ptr(k_hist), _ptr(ws), ws_bytes, ctypes.byref(steps),
-                                       _stream(stream)), "dcl_generate")
+    _check(load_library().dcl_generate(model, tp, B, S, pp, gen_end, kvp, score_flags, L, tau_commit,
+                                       tau_draft, select_flags, max_steps, check_every, _stats(stats, B * S, w),
+                                       _arg(k_raw, "k_raw", w, _I32, B), _arg(k_eff, "k_eff", w, _I32, B),
+                                       _arg(k_hist, "k_hist", w, _I32, L + 1 if L >= 0 else None),
+                                       _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes, ctypes.byref(steps),
+                                       _stream(stream)), w)
     del keep
     return steps.value
 
 
 def dcl_kv_append(model: int, tokens, B: int, S: int, kv, ws, ws_bytes: int, stream=None) -> None:
-    kvp, keep = _kv(kv)
-    _check(load_library().dcl_kv_append(model, _ptr(tokens), B, S, kvp, _ptr(ws), ws_bytes, _stream(stream)),
-           "dcl_kv_append")
+    w = "dcl_kv_append"
+    kvp, keep = _kv(kv, model, B, w)
+    _check(load_library().dcl_kv_append(model, _arg(tokens, "tokens", w, _I32, B * S), B, S, kvp,
+                                        _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes, _stream(stream)), w)
     del keep
 
 
@@ -223,16 +295,56 @@ def dcl_score_workspace_bytes(model: int, n: int) -> int:
 
 
 def dcl_score_hidden(model: int, hidden, n: int, stats, ws, ws_bytes: int, stream=None) -> None:
-    _check(load_library().dcl_score_hidden(model, _ptr(hidden), n, _stats(stats), _ptr(ws), ws_bytes,
-                                           _stream(stream)), "dcl_score_hidden")
+    w = "dcl_score_hidden"
+    g = _cfg_of(model)
+    _check(load_library().dcl_score_hidden(model, _arg(hidden, "hidden", w, _B16, n * g.d_model if g else None), n,
+                                           _stats(stats, n, w), _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes,
+                                           _stream(stream)), w)
 
 
 def dcl_debug_logits(model: int, tokens, B: int, S: int, kv, rows, n_rows: int, out, hidden_out, ws, ws_bytes: int,
                      stream=None) -> None:
-    kvp, keep = _kv(kv)
-    _check(load_library().dcl_debug_logits(model, _ptr(tokens), B, S, kvp, _ptr(rows), n_rows, _ptr(out),
-                                           _ptr(hidden_out), _ptr(ws), ws_bytes, _stream(stream)), "dcl_debug_logits")
+    w = "dcl_debug_logits"
+    g = _cfg_of(model)
+    kvp, keep = _kv(kv, model, B, w)
+    _check(load_library().dcl_debug_logits(
+        model, _arg(tokens, "tokens", w, _I32, B * S), B, S, kvp, _arg(rows, "rows", w, _I32, n_rows), n_rows,
+        _arg(out, "out", w, _F32, n_rows * g.vocab if g else None),
+        _arg(hidden_out, "hidden_out", w, _B16, n_rows * g.d_model if g else None),
+        _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes, _stream(stream)), w)
     del keep
+
+
+def dcl_debug_layer(model: int, B: int, S: int, kv, layer: int, r_in, taps: dict, ws, ws_bytes: int,
+                    stream=None) -> None:
+    """taps: dict name -> device tensor (names of DclLayerTaps; absent = not copied out)."""
+    w = "dcl_debug_layer"
+    g = _cfg_of(model)
+    T, Sp = B * S, (S + 7) // 8 * 8
+    size = {}
+    if g is not None:
+        hd, kd = g.n_heads * g.head_dim, g.n_kv_heads * g.head_dim
+        size = {"u": (_B16, T * g.d_model), "q": (_B16, T * hd), "k": (_B16, T * kd), "v": (_B16, B * kd * Sp),
+                "o": (_B16, T * hd), "r_mid": (_F32, T * g.d_model), "u2": (_B16, T * g.d_model),
+                "a": (_B16, T * g.d_ffn), "r_out": (_F32, T * g.d_model)}
+    unknown = set(taps) - {f for f, _ in DclLayerTaps._fields_}
+    if unknown:
+        raise DclError(1, w, f"unknown taps {sorted(unknown)}")
+    ct = DclLayerTaps(*(_arg(taps.get(f), f"taps[{f!r}]", w, *size.get(f, (_ANY, None)))
+                        for f, _ in DclLayerTaps._fields_))
+    kvp, keep = _kv(kv, model, B, w)
+    _check(load_library().dcl_debug_layer(model, B, S, kvp, layer,
+                                          _arg(r_in, "r_in", w, _F32, T * g.d_model if g else None), ct,
+                                          _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes, _stream(stream)), w)
+    del keep
+
+
+def dcl_debug_gemm_plan(Nw: int, T: int, K: int, lm_head: bool = False, max_split: int = 4) -> dict:
+    """The tile plan of a GEMM shape (host only): configuration, K-split slices and tile geometry."""
+    info = (ctypes.c_int32 * 8)()
+    _check(load_library().dcl_debug_gemm_plan(Nw, T, K, 1 if lm_head else 0, max_split, info), "dcl_debug_gemm_plan")
+    keys = ("cfg", "nsplit", "bw", "bt", "kd", "stages", "ww", "wt")
+    return dict(zip(keys, list(info)))
 
 
 # ---------------------------------------------------------------- convenience owner of device buffers

@@ -189,11 +189,11 @@ struct ProfScope {
 enum { P_EMBED, P_NORM, P_QKV, P_ATTN, P_O, P_GU, P_DOWN, P_COMPACT, P_LM, P_MERGE, P_SELECT };
 #define PROF(cls) ProfScope prof_scope_##__LINE__(cls, s)
 
-dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv, void* ws,
-                           size_t ws_bytes) {
+// Sizes, ranges and the cache description (host-only, no device access). Every check that depends
+// only on the arguments comes before the state check, so a call with bad sizes is reported as such
+// whether or not weights were loaded.
+dcl_status check_shape_args(const Model* m, int32_t B, int32_t S, const dcl_kv* kv) {
   if (!m) return fail(DCL_E_ARG, "model is NULL");
-  if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
-  if (!tokens) return fail(DCL_E_ARG, "tokens is NULL");
   if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
   if ((long)B * S > (1 << 22)) return fail(DCL_E_ARG, "B*S = %ld too large", (long)B * S);
   if ((long)B * (S + 8) * m->qkv_rows() >= (1L << 31))  // the QKV epilogue addresses q/k/v^T with 32 bits
@@ -215,6 +215,10 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   }
   if ((long)P + S > m->cfg.max_positions)
     return fail(DCL_E_ARG, "positions up to %ld exceed max_positions %d", (long)P + S, m->cfg.max_positions);
+  return DCL_OK;
+}
+
+dcl_status check_workspace(const Model* m, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
   if (!ws) return fail(DCL_E_ARG, "workspace is NULL");
   if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(DCL_E_ARG, "workspace must be 256-byte aligned");
   const size_t need = step_layout(m->cfg, B, S).total;
@@ -222,10 +226,27 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   return DCL_OK;
 }
 
-// a2-a7: embedding and every transformer layer. Returns the number of K-split slices of the last
-// residual GEMM still to be added to ws.r (the final RMSNorm folds them in).
-int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_kv* kv, void* ws,
-                 const StepLayout& L, hipStream_t s, bool writeback = false) {
+dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const dcl_kv* kv, void* ws,
+                           size_t ws_bytes) {
+  dcl_status st = check_shape_args(m, B, S, kv);
+  if (st != DCL_OK) return st;
+  if (!tokens) return fail(DCL_E_ARG, "tokens is NULL");
+  if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
+  return check_workspace(m, B, S, ws, ws_bytes);
+}
+
+// Device-to-device copy of a stage's result into a caller buffer (test support; null = not wanted).
+void tap(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  if (dst) (void)hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s);
+}
+
+// a3-a7 for layer l on the residual stream in ws.r. `pending` is the number of K-split slices of the
+// previous residual GEMM still to be added to ws.r (the first RMSNorm folds them in); the return value
+// is that number for this layer's down projection. With `writeback` the layer's fresh keys/values go
+// into the cache and the layer stops after them (returns -1). With `taps` every intermediate is also
+// copied out, and the down projection's slices are folded into ws.r before r_out is copied.
+int run_layer(const Model* m, int l, int B, int S, const dcl_kv* kv, void* ws, const StepLayout& L, hipStream_t s,
+              int pending, bool writeback = false, const dcl_layer_taps* taps = nullptr) {
   const dcl_config& c = m->cfg;
   const int T = B * S, d = c.d_model, dh = c.head_dim;
   const int P = kv ? kv->prefix_len : 0;
@@ -235,75 +256,106 @@ int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_k
   bf16_t* a = at<bf16_t>(ws, L.a);
   bf16_t* o = at<bf16_t>(ws, L.o);
   float* part = at<float>(ws, L.part);
+  const LayerOffsets& lo = m->lay.layer[l];
+  {
+    PROF(P_NORM);
+    launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, part, pending, s);
+  }
+  if (taps) tap(taps->u, u, (size_t)T * d * 2, s);
+  QkvOut qo;
+  qo.q = at<bf16_t>(ws, L.q);
+  qo.k = at<bf16_t>(ws, L.k);
+  qo.vt = at<bf16_t>(ws, L.vt);
+  qo.bias = c.qkv_bias ? at<float>(wb, lo.bqkv) : nullptr;
+  qo.rope = c.rope_enabled ? at<float2>(wb, m->lay.rope) : nullptr;
+  qo.H = c.n_heads;
+  qo.Hkv = c.n_kv_heads;
+  qo.dh = dh;
+  qo.S = S;
+  qo.Sp = L.Sp;
+  qo.pos0 = P;
+  {
+    PROF(P_QKV);
+    gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
+  }
+  if (taps) {
+    tap(taps->q, qo.q, (size_t)T * c.n_heads * dh * 2, s);
+    tap(taps->k, qo.k, (size_t)T * c.n_kv_heads * dh * 2, s);
+    tap(taps->v, qo.vt, (size_t)B * c.n_kv_heads * dh * L.Sp * 2, s);
+  }
+  if (writeback) {  // this layer's fresh keys and values into the cache at [P, P + S)
+    launch_kv_writeback(qo.k, qo.vt, static_cast<bf16_t*>(const_cast<void*>(kv->k[l])),
+                        static_cast<bf16_t*>(const_cast<void*>(kv->v[l])), B, c.n_kv_heads, S, L.Sp, dh, P,
+                        kv->capacity ? kv->capacity : P, s);
+    if (l == c.n_layers - 1) return -1;  // nothing after the last layer's keys and values is needed
+  }
+  AttnArgs aa;
+  aa.q = qo.q;
+  aa.k = qo.k;
+  aa.vt = qo.vt;
+  aa.kc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->k[l]) : nullptr;
+  aa.vc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->v[l]) : nullptr;
+  aa.o = o;
+  aa.B = B;
+  aa.H = c.n_heads;
+  aa.Hkv = c.n_kv_heads;
+  aa.dh = dh;
+  aa.S = S;
+  aa.Sp = L.Sp;
+  aa.P = P;
+  aa.Pc = kv ? (kv->capacity ? kv->capacity : P) : 0;
+  aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
+  {
+    PROF(P_ATTN);
+    launch_attention(aa, s);
+  }
+  if (taps) tap(taps->o, o, (size_t)T * c.n_heads * dh * 2, s);
+  {
+    PROF(P_O);
+    pending = gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, part, s);
+  }
+  {
+    PROF(P_NORM);
+    launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, part, pending, s);
+  }
+  if (taps) {
+    tap(taps->r_mid, r, (size_t)T * d * 4, s);
+    tap(taps->u2, u, (size_t)T * d * 2, s);
+  }
+  {
+    PROF(P_GU);
+    gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
+  }
+  if (taps) tap(taps->a, a, (size_t)T * c.d_ffn * 2, s);
+  {
+    PROF(P_DOWN);
+    pending = gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, part, s);
+  }
+  if (taps) {
+    // fold the down projection's slices into r exactly as the next RMSNorm would (same kernel, same
+    // split order); its normalised output goes to the h_f scratch and is not used
+    if (pending > 0)
+      launch_rmsnorm(r, at<float>(wb, m->lay.gf), at<bf16_t>(ws, L.hf), T, d, c.rms_eps, nullptr, nullptr, part,
+                     pending, s);
+    pending = 0;
+    tap(taps->r_out, r, (size_t)T * d * 4, s);
+  }
+  return pending;
+}
+
+// a2-a7: embedding and every transformer layer. Returns the number of K-split slices of the last
+// residual GEMM still to be added to ws.r (the final RMSNorm folds them in).
+int run_forward(const Model* m, const int32_t* tokens, int B, int S, const dcl_kv* kv, void* ws,
+                const StepLayout& L, hipStream_t s, bool writeback = false) {
+  const dcl_config& c = m->cfg;
   int pending = 0;  // K-split slices of the last residual GEMM not yet added to r
   {
     PROF(P_EMBED);
-    launch_embed(tokens, at<bf16_t>(wb, m->lay.embed), r, T, d, c.vocab, s);
+    launch_embed(tokens, at<bf16_t>(m->wbuf, m->lay.embed), at<float>(ws, L.r), B * S, c.d_model, c.vocab, s);
   }
   for (int l = 0; l < c.n_layers; ++l) {
-    const LayerOffsets& lo = m->lay.layer[l];
-    {
-      PROF(P_NORM);
-      launch_rmsnorm(r, at<float>(wb, lo.g1), u, T, d, c.rms_eps, nullptr, nullptr, part, pending, s);
-    }
-    QkvOut qo;
-    qo.q = at<bf16_t>(ws, L.q);
-    qo.k = at<bf16_t>(ws, L.k);
-    qo.vt = at<bf16_t>(ws, L.vt);
-    qo.bias = c.qkv_bias ? at<float>(wb, lo.bqkv) : nullptr;
-    qo.rope = c.rope_enabled ? at<float2>(wb, m->lay.rope) : nullptr;
-    qo.H = c.n_heads;
-    qo.Hkv = c.n_kv_heads;
-    qo.dh = dh;
-    qo.S = S;
-    qo.Sp = L.Sp;
-    qo.pos0 = P;
-    {
-      PROF(P_QKV);
-      gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
-    }
-    if (writeback) {  // this layer's fresh keys and values into the cache at [P, P + S)
-      launch_kv_writeback(qo.k, qo.vt, static_cast<bf16_t*>(const_cast<void*>(kv->k[l])),
-                          static_cast<bf16_t*>(const_cast<void*>(kv->v[l])), B, c.n_kv_heads, S, L.Sp, dh, P,
-                          kv->capacity ? kv->capacity : P, s);
-      if (l == c.n_layers - 1) break;  // nothing after the last layer's keys and values is needed
-    }
-    AttnArgs aa;
-    aa.q = qo.q;
-    aa.k = qo.k;
-    aa.vt = qo.vt;
-    aa.kc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->k[l]) : nullptr;
-    aa.vc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->v[l]) : nullptr;
-    aa.o = o;
-    aa.B = B;
-    aa.H = c.n_heads;
-    aa.Hkv = c.n_kv_heads;
-    aa.dh = dh;
-    aa.S = S;
-    aa.Sp = L.Sp;
-    aa.P = P;
-    aa.Pc = kv ? (kv->capacity ? kv->capacity : P) : 0;
-    aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
-    {
-      PROF(P_ATTN);
-      launch_attention(aa, s);
-    }
-    {
-      PROF(P_O);
-      pending = gemm_resid(at<bf16_t>(wb, lo.wo), o, d, T, c.n_heads * dh, r, part, s);
-    }
-    {
-      PROF(P_NORM);
-      launch_rmsnorm(r, at<float>(wb, lo.g2), u, T, d, c.rms_eps, nullptr, nullptr, part, pending, s);
-    }
-    {
-      PROF(P_GU);
-      gemm_swiglu(at<bf16_t>(wb, lo.wgu), u, 2 * c.d_ffn, T, d, a, s);
-    }
-    {
-      PROF(P_DOWN);
-      pending = gemm_resid(at<bf16_t>(wb, lo.wd), a, d, T, c.d_ffn, r, part, s);
-    }
+    pending = run_layer(m, l, B, S, kv, ws, L, s, pending, writeback);
+    if (pending < 0) return 0;
   }
   return pending;
 }
@@ -739,6 +791,38 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
     if (st != DCL_OK) return st;
   }
   return hip_check(hipGetLastError(), "debug_logits launch");
+}
+
+dcl_status dcl_debug_layer(dcl_model_t model, int32_t B, int32_t S, const dcl_kv* kv, int32_t layer,
+                           const float* r_in, dcl_layer_taps taps, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  dcl_status st = check_shape_args(m, B, S, kv);
+  if (st != DCL_OK) return st;
+  if (layer < 0 || layer >= m->cfg.n_layers) return fail(DCL_E_ARG, "layer %d outside [0, %d)", layer, m->cfg.n_layers);
+  if (!r_in) return fail(DCL_E_ARG, "r_in is NULL");
+  if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
+  st = check_workspace(m, B, S, ws, ws_bytes);
+  if (st != DCL_OK) return st;
+  const StepLayout L = step_layout(m->cfg, B, S);
+  (void)hipGetLastError();
+  st = hip_check(hipMemcpyAsync(at<float>(ws, L.r), r_in, (size_t)B * S * m->cfg.d_model * 4, hipMemcpyDeviceToDevice,
+                                stream), "hipMemcpyAsync(r_in)");
+  if (st != DCL_OK) return st;
+  run_layer(m, layer, B, S, kv, ws, L, stream, 0, false, &taps);
+  return hip_check(hipGetLastError(), "debug_layer launch");
+}
+
+dcl_status dcl_debug_gemm_plan(int32_t Nw, int32_t T, int32_t K, int32_t lm_head, int32_t max_split, int32_t* info) {
+  if (!info) return fail(DCL_E_ARG, "info is NULL");
+  if (Nw < 1 || T < 1 || K < 1 || max_split < 1 || max_split > kMaxSplit)
+    return fail(DCL_E_ARG, "Nw=%d T=%d K=%d max_split=%d outside their ranges", Nw, T, K, max_split);
+  const GemmPlan p = plan_gemm(Nw, T, K, lm_head ? kLmTile : 0, lm_head ? 1 : max_split);
+  int shape[6];
+  gemm_cfg_shape(p.cfg, shape);
+  info[0] = p.cfg;
+  info[1] = p.nsplit;
+  for (int i = 0; i < 6; ++i) info[2 + i] = shape[i];
+  return DCL_OK;
 }
 
 dcl_status dcl_profile_enable(int32_t on) {

@@ -125,6 +125,8 @@ struct GemmPlan {
 };
 // force_bw: restrict to tiles of that many weight rows (0: any); max_split: largest K-split factor.
 GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split);
+// Tile of configuration `cfg`: {weight rows, tokens, K depth per stage, stages, waves along W, waves along T}.
+void gemm_cfg_shape(int cfg, int* shape);
 constexpr int kMaxSplit = 4;  // K-split slices of the residual GEMMs
 void gemm_qkv(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const QkvOut& o, hipStream_t s);
 // r += W X^T, either in place (returns 0) or as n float32 slices P[s][T][Nw] that the next RMSNorm

@@ -700,6 +700,16 @@ GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
   return best;
 }
 
+void gemm_cfg_shape(int cfg, int* shape) {
+  const TileCfg& c = kCfgs[cfg >= 0 && cfg < kNumCfgs ? cfg : 0];
+  shape[0] = c.bw;
+  shape[1] = c.bt;
+  shape[2] = c.kd;
+  shape[3] = c.stages;
+  shape[4] = c.ww;
+  shape[5] = c.wt;
+}
+
 template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi>
 static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
                     const Epi& epi, hipStream_t s) {
