@@ -43,6 +43,19 @@ def runner_for(workload, stored, max_positions=None, rope=True):
     return Runner(workload.geom, tensors, max_positions=mp, rope_enabled=rope)
 
 
+_FULL = {}
+
+
+def full_runner(workload):
+    """(stored weights, Runner) of a full-size geometry, shared by every test module of one pytest process
+    (each 7-8B model holds about 16 GB on the host and on the GPU; both geometries stay loaded)."""
+    name = workload.geom.name
+    if name not in _FULL:
+        stored = synth.make_weights(workload.geom)
+        _FULL[name] = (stored, runner_for(workload, stored, max_positions=4096))
+    return _FULL[name]
+
+
 def to_dev(a, dtype=None):
     import torch
     t = torch.from_numpy(np.ascontiguousarray(a))

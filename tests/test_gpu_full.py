@@ -18,12 +18,11 @@ import pytest
 import oracle
 import synth
 
-from helpers import CONF_TOL, DRIFT_FACTOR, LOGIT_TOL, runner_for, stats_to_np, to_dev
+from helpers import CONF_TOL, DRIFT_FACTOR, LOGIT_TOL, full_runner, stats_to_np, to_dev
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-_runners = {}
 
 
 def _golden(key):
@@ -35,18 +34,11 @@ def _golden(key):
 
 def _runner(w, gold):
     import hashlib
-    import torch
-    name = w.geom.name
-    if name not in _runners:
-        _runners.clear()
-        torch.cuda.empty_cache()
-        stored = synth.make_weights(w.geom)
-        for n, h in zip(gold["checksum_names"], gold["checksum_values"]):
-            got = hashlib.sha256(np.ascontiguousarray(stored[str(n)]).tobytes()).hexdigest()[:16]
-            assert got == str(h), f"regenerated weight {n} differs from the one the golden values used"
-        _runners[name] = runner_for(w, stored)
-        del stored
-    return _runners[name]
+    stored, run = full_runner(w)
+    for n, h in zip(gold["checksum_names"], gold["checksum_values"]):
+        got = hashlib.sha256(np.ascontiguousarray(stored[str(n)]).tobytes()).hexdigest()[:16]
+        assert got == str(h), f"regenerated weight {n} differs from the one the golden values used"
+    return run
 
 
 @pytest.mark.parametrize("key", ["c2", "c3", "c5", "c4"])
