@@ -29,7 +29,7 @@ CONF_TOL = 1e-3        # max-abs on confidences (exact-input bar)
 LOGIT_TOL = 2e-2       # max-abs on float32 logits vs float64 oracle logits (exact-input bar)
 NEAR = 1e-3            # |conf - tau| below this is reported separately
 TIE_GAP = 4e-2         # logit gap below this: the top-1 id may legitimately flip (exact inputs)
-DRIFT_FACTOR = 4.0     # whole-step tolerance = DRIFT_FACTOR * float32-evaluation drift
+DRIFT_FACTOR = 3.0     # whole-step tolerance = DRIFT_FACTOR * float32-evaluation drift
 FEW_ROWS = 16          # below this many scored rows the drift is sampled over ORDERS orders
 ORDERS = 32
 

@@ -132,3 +132,46 @@ def test_binding_flag_constants_match_header():
             "DCL_SEL_CONTIGUOUS_DRAFTS"} <= set(defs)
     for name, val in defs.items():
         assert getattr(b, name) == int(val, 16), name
+
+
+def test_step_size_limits_rejected_on_the_host(dcl):
+    """The 32-bit offset limits of dcl_denoise_step are checked before the weights-loaded state and before
+    any HIP call: one 4096-token sequence more than the largest accepted batch of the small model (q/k/v^T
+    would reach 2^31 elements), B*S above 2^22, and FFN activations of 2^31 elements."""
+    import dataclasses
+    lib = dcl.load_library()
+    st = dcl.binding.DclRowStats(256, 256, 256, 256, 256)
+
+    def step(cfg, B, S):
+        m = dcl.dcl_model_create(cfg)
+        try:
+            r = lib.dcl_denoise_step(m, 256, B, S, 256, S, None, 0, st, 256, 1 << 40, None)
+            return r, dcl.dcl_last_error()
+        finally:
+            dcl.dcl_model_destroy(m)
+
+    tiny = dcl.config_from_geometry(synth.TINY, max_positions=4096)
+    g = synth.TINY
+    qkv_rows = (g.n_heads + 2 * g.n_kv_heads) * g.head_dim
+    assert 681 * (4096 + 8) * qkv_rows < 2 ** 31 <= 682 * (4096 + 8) * qkv_rows
+    r, msg = step(tiny, 682, 4096)
+    assert r == 2 and "q/k/v" in msg
+    r, msg = step(tiny, 681, 4096)
+    assert r == 5 and "not loaded" in msg            # within the limits: only the state check remains
+    r, msg = step(tiny, 1025, 4096)
+    assert r == 1 and "too large" in msg
+    wide = dcl.config_from_geometry(dataclasses.replace(g, n_layers=1, d_model=64, n_heads=1, n_kv_heads=1,
+                                                        head_dim=64, d_ffn=65536, vocab=256, mask_id=255),
+                                    max_positions=4096)
+    r, msg = step(wide, 8, 4096)
+    assert r == 2 and "activation" in msg
+
+
+def test_binding_rejects_host_tensors_before_calling_the_library(dcl):
+    """The binding checks tensor arguments (device, dtype, size) and raises before the C call."""
+    import torch
+    tok = torch.zeros((1, 8), dtype=torch.int32)
+    with pytest.raises(dcl.DclError) as e:
+        dcl.dcl_select_contiguous(tok, 1, 8, 256, 8, 4, 0.7, 0.98, 3, {"top1": 256, "conf": 256})
+    assert e.value.status == 1 and "device" in str(e.value)
+

@@ -7,8 +7,12 @@ the GPU's confidence / log-sum-exp differences from the float64 oracle must stay
 DRIFT_FACTOR times that evaluation's differences, both in the maximum and in the median (the median
 is the sharper check: most rows are far from any rounding flip). Token ids may differ only where the
 oracle's top-1/top-2 logit gap is below the logit tolerance. Selections are bit-exact given the GPU
-statistics, and the acceptance length K equals the oracle's unless a window row lies within the
-confidence tolerance of the threshold.
+statistics. Every acceptance length K that differs from the oracle's is reported with its deciding
+row (oracle confidence, distance from the threshold, the GPU's and the float32 evaluation's
+confidence there); such a row must lie within the step's confidence tolerance of the threshold.
+
+The stated bar (confidences within 1e-3, logits within 2e-2, ids and K bit-exact away from the
+threshold) is met stage by stage, on identical stage inputs, in test_gpu_layers.py.
 """
 import os
 
@@ -87,7 +91,7 @@ def test_full_size_step(key):
     assert np.median(dlse) <= DRIFT_FACTOR * np.median(flse) + 1e-6
     assert not (mism & ~tie).any(), f"top1 differs outside near-tie rows: {np.nonzero(mism & ~tie)[0][:10]}"
 
-    # selection on the GPU statistics: bit-exact against the oracle's rule; K against the oracle's K
+    # selection on the GPU statistics: bit-exact against the oracle's rule
     k_raw = torch.zeros(B, dtype=torch.int32, device="cuda")
     k_eff = torch.zeros(B, dtype=torch.int32, device="cuda")
     dcl.dcl_select_contiguous(t_dev, B, S, p_dev, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id, st_dev,
@@ -98,14 +102,37 @@ def test_full_size_step(key):
     np.testing.assert_array_equal(t_dev.cpu().numpy(), x_ref)
     np.testing.assert_array_equal(p_dev.cpu().numpy(), p_ref)
     np.testing.assert_array_equal(k_raw.cpu().numpy(), kr_ref)
-    oracle_conf = np.full(B * S, -1.0)
-    oracle_conf[rows] = gold["conf"]
-    oracle_conf = oracle_conf.reshape(B, S)
+    # acceptance lengths against the oracle's: every difference is reported with its deciding row (the first
+    # window row where the GPU's and the oracle's conf > tau decisions differ), its oracle confidence and
+    # distance from tau, and what the float32 evaluation of the definition decided there
+    gconf = gpu["conf"].astype(np.float64)
+    oconf = np.full(B * S, -1.0)
+    oconf[rows] = gold["conf"]
+    oconf = oconf.reshape(B, S)
+    fconf_all = np.full(B * S, -1.0)
+    fconf_all[rows] = gold["f32_conf"]
+    fconf_all = fconf_all.reshape(B, S)
+    k_gpu = k_raw.cpu().numpy()
+    ftop = np.full(B * S, -1, np.int64)
+    ftop[rows] = gold["f32_top1"]
+    _, _, k_f32, _ = oracle.select_contiguous(tok, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id,
+                                              ftop.reshape(B, S), fconf_all)
+    mismatches = []
     for b in range(B):
-        pb = int(p[b])
-        win = oracle_conf[b, pb:pb + min(w.window, w.gen_end - pb)]
-        near = bool((np.abs(win - w.tau_commit) < conf_tol).any())
-        got_k = int(k_raw[b].item())
-        print(f"  seq {b}: K oracle {int(gold['sel_k_raw'][b])}, GPU {got_k}, near-threshold window: {near}", flush=True)
-        if not near:
-            assert got_k == int(gold["sel_k_raw"][b])
+        ko, kg, kf = int(gold["sel_k_raw"][b]), int(k_gpu[b]), int(k_f32[b])
+        line = f"  seq {b}: K oracle {ko}, GPU {kg}, float32 evaluation {kf}"
+        if kg != ko:
+            j = int(p[b]) + min(kg, ko)
+            rec = dict(seq=b, k_oracle=ko, k_gpu=kg, k_float32=kf, row=j, oracle_conf=float(oconf[b, j]),
+                       dist_tau=float(abs(oconf[b, j] - w.tau_commit)), gpu_conf=float(gconf[b, j]),
+                       float32_conf=float(fconf_all[b, j]))
+            mismatches.append(rec)
+            line += (f"  <- deciding row {j}: oracle conf {rec['oracle_conf']:.4f} (|c - tau| = {rec['dist_tau']:.4f}),"
+                     f" GPU {rec['gpu_conf']:.4f}, float32 evaluation {rec['float32_conf']:.4f}")
+        print(line, flush=True)
+    print(f"{key}: {len(mismatches)} of {B} acceptance lengths differ from the oracle's; the float32 evaluation of the "
+          f"definition differs in {int((k_f32 != gold['sel_k_raw']).sum())}", flush=True)
+    for m in mismatches:
+        # a whole step can only move K through a window row whose confidence crossed tau, which needs the row
+        # within the step's confidence tolerance of tau
+        assert m["dist_tau"] <= conf_tol, f"K differs with the deciding row {m['dist_tau']:.3g} from tau: {m}"
