@@ -157,6 +157,22 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
                             const int32_t* p, int32_t gen_end, const dcl_kv* kv, uint32_t flags,
                             dcl_row_stats out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): dcl_denoise_step with its workspace taken from a static scratch
+ * array of DCL_NOALLOC_SCRATCH_BYTES bytes inside the library, one per device, held until the process
+ * ends. The call allocates nothing (no hipMalloc / hipFree, no allocating library routine); the first
+ * call on a device looks up that device's scratch address (hipGetSymbolAddress) and keeps it. Steps
+ * whose workspace (dcl_workspace_bytes) exceeds the scratch are rejected with DCL_E_WORKSPACE before
+ * anything is launched (the LLaDA-8B geometry fits B*S = 384 tokens, and B = 8 x 64 tokens after a
+ * cached prefix). Every call on a device shares that device's scratch: calls that overlap in time on
+ * one device (two streams, two threads) race and give undefined results; calls ordered on one stream
+ * are safe. Nothing in the scratch needs to start at zero (every step writes what it reads). Uses the
+ * current device; `stream` must belong to it. Other arguments, results and errors as dcl_denoise_step. */
+#define DCL_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
+dcl_status dcl_denoise_step_noalloc(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
+                                    const int32_t* p, int32_t gen_end, const dcl_kv* kv, uint32_t flags,
+                                    dcl_row_stats out, hipStream_t stream);
+
 /* Steps (iii), (iv) and (i) for every sequence b with p[b] < gen_end, in place on tokens [B, S]
  * and p [B] (device), using statistics `in` of a dcl_denoise_step on the same tokens:
  *   L_eff = min(L, gen_end - p);  K = number of leading window rows with conf > tau_commit

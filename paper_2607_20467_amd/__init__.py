@@ -14,3 +14,4 @@ from .binding import (  # noqa: F401
     dcl_workspace_bytes, library_path, load_library,
 )
 from . import binding  # noqa: F401,E402
+from .binding import DCL_NOALLOC_SCRATCH_BYTES, dcl_denoise_step_noalloc  # noqa: F401,E402

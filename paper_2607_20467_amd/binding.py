@@ -89,6 +89,8 @@ def load_library():
         "dcl_workspace_bytes": (sz, [vp, i32, i32, i32]),
         "dcl_denoise_step": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, DclRowStats,
                                             vp, sz, vp]),
+        "dcl_denoise_step_noalloc": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32,
+                                                    DclRowStats, vp]),
         "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, f32, f32, i32, DclRowStats, vp, vp,
                                                  u32, vp]),
         "dcl_generate": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, i32, f32, f32, u32,
@@ -241,6 +243,19 @@ def dcl_denoise_step(model: int, tokens, B: int, S: int, p, gen_end: int, kv, fl
     tp, pp = _state(tokens, p, B, S, w)
     _check(load_library().dcl_denoise_step(model, tp, B, S, pp, gen_end, kvp, flags, _stats(stats, B * S, w),
                                            _arg(ws, "ws", w, _ANY, nbytes=ws_bytes), ws_bytes, _stream(stream)), w)
+    del keep
+
+
+DCL_NOALLOC_SCRATCH_BYTES = 96 << 20
+
+
+def dcl_denoise_step_noalloc(model: int, tokens, B: int, S: int, p, gen_end: int, kv, flags: int, stats,
+                             stream=None) -> None:
+    w = "dcl_denoise_step_noalloc"
+    kvp, keep = _kv(kv, model, B, w)
+    tp, pp = _state(tokens, p, B, S, w)
+    _check(load_library().dcl_denoise_step_noalloc(model, tp, B, S, pp, gen_end, kvp, flags,
+                                                   _stats(stats, B * S, w), _stream(stream)), w)
     del keep
 
 

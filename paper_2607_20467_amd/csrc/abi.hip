@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -431,6 +432,34 @@ dcl_status check_select_args(const int32_t* tokens, int32_t B, int32_t S, const 
   return DCL_OK;
 }
 
+// Scratch of dcl_denoise_step_noalloc: a fixed device array in the library's code object, one copy per
+// device (each device that runs the call holds it until the process ends). Host code never uses the
+// array's name as an address: the device address comes from hipGetSymbolAddress, taken once per device
+// with that device current, and kernels receive that address as their workspace pointer.
+static __device__ __align__(256) unsigned char scratch[DCL_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the current device's scratch (looked up on the first call per device).
+dcl_status scratch_address(void** out) {
+  int dev = -1;
+  dcl_status st = hip_check(hipGetDevice(&dev), "hipGetDevice");
+  if (st != DCL_OK) return st;
+  if (dev < 0 || dev >= kMaxDevices) return fail(DCL_E_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    st = hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (st != DCL_OK) return st;
+    if (!p || (reinterpret_cast<uintptr_t>(p) & 255) != 0) return fail(DCL_E_HIP, "scratch address %p not 256-byte aligned", p);
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return DCL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -574,6 +603,27 @@ dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B,
   enqueue_denoise(m, tokens, B, S, p, gen_end, kv, flags, out, ws, stream);
   return hip_check(hipGetLastError(), "denoise_step launch");
 }
+dcl_status dcl_denoise_step_noalloc(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S, const int32_t* p,
+                                    int32_t gen_end, const dcl_kv* kv, uint32_t flags, dcl_row_stats out,
+                                    hipStream_t stream) {
+  Model* m = reinterpret_cast<Model*>(model);
+  dcl_status st = check_shape_args(m, B, S, kv);
+  if (st != DCL_OK) return st;
+  const size_t need = step_layout(m->cfg, B, S).total;
+  if (need > (size_t)DCL_NOALLOC_SCRATCH_BYTES)
+    return fail(DCL_E_WORKSPACE, "B=%d, S=%d needs %zu bytes of scratch; the static scratch holds %zu (use "
+                "dcl_denoise_step with a workspace)", B, S, need, (size_t)DCL_NOALLOC_SCRATCH_BYTES);
+  if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != DCL_OK) return st;
+  st = check_denoise_args(m, tokens, B, S, p, gen_end, kv, flags, out, ws, (size_t)DCL_NOALLOC_SCRATCH_BYTES);
+  if (st != DCL_OK) return st;
+  (void)hipGetLastError();
+  enqueue_denoise(m, tokens, B, S, p, gen_end, kv, flags, out, ws, stream);
+  return hip_check(hipGetLastError(), "denoise_step_noalloc launch");
+}
+
 dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end, int32_t L,
                                  float tau_commit, float tau_draft, int32_t mask_id, dcl_row_stats in,
                                  int32_t* K_raw, int32_t* K_eff, uint32_t flags, hipStream_t stream) {

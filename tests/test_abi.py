@@ -175,3 +175,19 @@ def test_binding_rejects_host_tensors_before_calling_the_library(dcl):
         dcl.dcl_select_contiguous(tok, 1, 8, 256, 8, 4, 0.7, 0.98, 3, {"top1": 256, "conf": 256})
     assert e.value.status == 1 and "device" in str(e.value)
 
+
+def test_noalloc_step_rejects_sizes_beyond_its_scratch_on_the_host(dcl):
+    """dcl_denoise_step_noalloc refuses a step whose workspace exceeds the static scratch before the
+    weights-loaded state and before any HIP call."""
+    lib = dcl.load_library()
+    m = dcl.dcl_model_create(dcl.config_from_geometry(synth.LLADA8B, max_positions=4096))
+    try:
+        st = dcl.binding.DclRowStats(256, 256, 256, 256, 256)
+        assert dcl.dcl_workspace_bytes(m, 1, 384, 0) <= dcl.DCL_NOALLOC_SCRATCH_BYTES
+        assert dcl.dcl_workspace_bytes(m, 1, 1280, 0) > dcl.DCL_NOALLOC_SCRATCH_BYTES
+        r = lib.dcl_denoise_step_noalloc(m, 256, 1, 1280, 256, 1280, None, 0, st, None)
+        assert r == 3 and "static scratch" in dcl.dcl_last_error()
+        r = lib.dcl_denoise_step_noalloc(m, 256, 1, 384, 256, 384, None, 0, st, None)
+        assert r == 5 and "not loaded" in dcl.dcl_last_error()
+    finally:
+        dcl.dcl_model_destroy(m)
