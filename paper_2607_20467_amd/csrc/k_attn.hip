@@ -62,9 +62,9 @@ __device__ __forceinline__ void attn_wait_stages(int newer) {
 
 // K and V^T tiles move HBM/L2 -> LDS with global_load_lds_dwordx4 into a STAGES-deep ring (no
 // register staging, no padding). K rows (DH/8 chunks of 16 bytes) are XOR-swizzled by the key
-// index, V^T rows (KT/8 chunks of 8 keys) by the dimension index. The 16-byte K fragment reads are
-// bank-conflict free; the 8-byte V^T reads see two-way conflicts (the 16 lanes of a pass read the
-// same half of 8 distinct chunks). Chunks past the last key repeat real data (see below).
+// index, V^T rows (KT/8 chunks of 8 keys) by the dimension index. Both are read in whole 16-byte
+// chunks, bank-conflict free; the V^T fragments are then assembled by a lane-row swap (below).
+// Chunks past the last key repeat real data (see below).
 //
 // Key groups: the NQ * KG waves of a workgroup are NQ query waves (16 queries each) times KG key
 // groups. Step t of the ring holds the KG key tiles t*KG .. t*KG + KG - 1; key group g works on
@@ -221,17 +221,23 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
         for (int kt = 0; kt < KT / 16; ++kt) sc[kt] = mfma16a(kfr[kt][ks], qf[ks], sc[kt]);
       // V^T fragments, read while the softmax below runs: dimension 16 dt + lq at the keys
       // 32 s2 + 4 lg + {0..3} and 32 s2 + 16 + 4 lg + {0..3} (the order in which the score MFMA left
-      // the probabilities in the lanes)
+      // the probabilities in the lanes). Each lane reads one whole 16-byte chunk (bank-conflict free
+      // through the XOR swizzle, as the K reads): lane groups 0 / 1 / 2 / 3 read the keys
+      // 0-7 / 16-23 / 8-15 / 24-31 of the 32-key block, and neighbouring groups (0, 1) and (2, 3)
+      // exchange halves with v_permlane16_swap, which swaps the odd 16-lane rows of its first operand
+      // with the even rows of its second: group 0 keeps keys 0-3 and receives 16-19, group 1 receives
+      // 4-7 and keeps 20-23, and likewise for groups 2 and 3.
       bf16x8_t vfr[KT / 32][DH / 16];
 #pragma unroll
       for (int s2 = 0; s2 < KT / 32; ++s2) {
-        const int c0 = 4 * s2 + (lg >> 1), c1 = c0 + 2, half = lg & 1;
+        const int cx = 4 * s2 + (((lg & 1) << 1) | (lg >> 1));
 #pragma unroll
         for (int dt = 0; dt < DH / 16; ++dt) {
           const int d = 16 * dt + lq;
-          const uint2 v0 = reinterpret_cast<const uint2*>(sV + d * VC + (c0 ^ (d & (VC - 1))))[half];
-          const uint2 v1 = reinterpret_cast<const uint2*>(sV + d * VC + (c1 ^ (d & (VC - 1))))[half];
-          vfr[s2][dt] = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+          const uint4 x = sV[d * VC + (cx ^ (d & (VC - 1)))];
+          const auto s0 = __builtin_amdgcn_permlane16_swap(x.x, x.z, false, false);
+          const auto s1 = __builtin_amdgcn_permlane16_swap(x.y, x.w, false, false);
+          vfr[s2][dt] = __builtin_bit_cast(bf16x8_t, make_uint4(s0[0], s1[0], s0[1], s1[1]));
         }
       }
       if (k0 + KT > nkeys) {  // only the last tile holds keys past the end
