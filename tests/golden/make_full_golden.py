@@ -5,7 +5,8 @@ top1 / top2 / conf / p2 / lse, the drift of the same definition evaluated in flo
 the whole-step tolerance), the oracle's selection on its own statistics, and checksums of a few
 weight tensors so a machine that regenerates different weights is detected.
 
-    python tests/golden/make_full_golden.py [c2 c3 c4 c5]     (about 10 minutes on 8 cores)
+    python tests/golden/make_full_golden.py [--out DIR] [c2 c3 c4 c5]
+(tens of minutes on 8 cores; DIR defaults to this directory)
 """
 import hashlib
 import os
@@ -28,6 +29,9 @@ def checksums(stored):
     return {n: hashlib.sha256(np.ascontiguousarray(stored[n]).tobytes()).hexdigest()[:16] for n in CHECK_TENSORS}
 
 
+OUT = HERE
+
+
 def run(key, stored):
     w = synth.WORKLOADS[key]
     g = w.geom
@@ -41,10 +45,23 @@ def run(key, stored):
             return synth.bf16_bits_to_f32(k[b]), synth.bf16_bits_to_f32(v[b])
         kv.prefix = w.kv_prefix
     W = WeightView(stored)
+
+    def per_sequence(**kw):
+        """oracle.step one sequence at a time (the same result; a progress line after each)."""
+        parts = []
+        for b in range(tok.shape[0]):
+            kvb = None
+            if kv is not None:
+                kvb = lambda bb, l, b=b: kv(b, l)
+                kvb.prefix = kv.prefix
+            parts.append(oracle.step(g, W, tok[b:b + 1], p[b:b + 1], w.gen_end, kv=kvb, **kw))
+            print(f"  {key} sequence {b} ({kw.get('dtype', np.float64).__name__}) done", flush=True)
+        return {k: np.concatenate([q[k] for q in parts]) for k in parts[0]}
+
     t0 = time.time()
-    ref = oracle.step(g, W, tok, p, w.gen_end, kv=kv)
+    ref = per_sequence()
     t1 = time.time()
-    f32 = oracle.step(g, W, tok, p, w.gen_end, kv=kv, dtype=np.float32)
+    f32 = per_sequence(dtype=np.float32)
     t2 = time.time()
     m = ref["conf"] >= 0
     rows = np.nonzero(m.reshape(-1))[0]
@@ -65,7 +82,7 @@ def run(key, stored):
                sel_tokens=x, sel_p=pn, sel_k_raw=kr, sel_k_eff=ke, f32_sel_k_raw=kr32,
                checksum_names=np.array(CHECK_TENSORS), checksum_values=np.array([checksums(stored)[n] for n in CHECK_TENSORS]),
                oracle_seconds=np.float64(t1 - t0))
-    np.savez_compressed(os.path.join(HERE, f"full_{key}.npz"), **out)
+    np.savez_compressed(os.path.join(OUT, f"full_{key}.npz"), **out)
     print(f"{key}: {len(rows)} scored rows, oracle {t1 - t0:.0f} s, float32 evaluation {t2 - t1:.0f} s, "
           f"drift conf {out['drift_conf']:.3g} lse {out['drift_lse']:.3g}, K_eff {ke.tolist()}, "
           f"K of the float32 evaluation {kr32.tolist()}", flush=True)
@@ -84,4 +101,9 @@ def main(keys):
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:] or ["c2", "c3", "c5", "c4"])
+    args = sys.argv[1:]
+    if args[:1] == ["--out"]:
+        OUT = args[1]
+        os.makedirs(OUT, exist_ok=True)
+        args = args[2:]
+    main(args or ["c2", "c3", "c5", "c4"])
