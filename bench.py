@@ -132,19 +132,22 @@ def pmc_summary(csv_path, copy_mib):
 
 
 def gpu_clock_mhz():
-    """Current shader clock reported by rocm-smi right after the timed steps (None if unavailable).
-    Not read under rocprofv3: its preloaded tool would initialise the GPU inside the rocm-smi child,
-    which then replaces itself with the Python interpreter."""
+    """Current shader clock (MHz) read from the amdgpu driver's sysfs table right after the timed steps: the
+    level marked '*' in pp_dpm_sclk of the first card that has one (None if unreadable). A file read, so
+    nothing is started from the process that holds the GPU."""
+    import glob
     import re
-    import subprocess
-    if any(k.startswith("ROCPROF") for k in os.environ):
-        return None
-    try:
-        out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20).stdout
-    except Exception:
-        return None
-    m = re.search(r"sclk clock level:\s*\d+:\s*\((\d+)\s*Mhz\)", out, re.IGNORECASE)
-    return int(m.group(1)) if m else None
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            with open(path) as f:
+                for line in f:
+                    if "*" in line:
+                        m = re.search(r"(\d+)\s*Mhz", line, re.IGNORECASE)
+                        if m:
+                            return int(m.group(1))
+        except OSError:
+            continue
+    return None
 
 
 def step_flops(w, R):
@@ -153,32 +156,69 @@ def step_flops(w, R):
     return L * sum(v for k, v in per.items() if k != "gemm_lm_head_top2") + per["gemm_lm_head_top2"]
 
 
-def cpu_baseline(w, stored, tok, p, R, layers_sample=8, rows_sample=64):
-    """The float64 oracle on a bounded sample of the same step, scaled to one full step."""
+def host_description():
+    """Host CPU model, logical CPUs, and the BLAS library numpy uses with its thread count."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas, threads = None, None
+    try:
+        from threadpoolctl import threadpool_info
+        for info in threadpool_info():
+            if info.get("user_api") == "blas":
+                blas = f"{info.get('internal_api')} {info.get('version')}"
+                threads = info.get("num_threads")
+                break
+    except Exception:
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "blas": blas, "blas_threads": threads}
+
+
+def cpu_baseline(w, stored, tok, p, R, kv_host=None, full=True, layers_sample=8, rows_sample=64):
+    """The float64 oracle on the same step, timed on the host. With ``full`` one whole oracle step (forward
+    of every sequence over every layer, statistics of every scored row); otherwise a sample (the forward over
+    ``layers_sample`` layers and the statistics of ``rows_sample`` rows) scaled to one step."""
     import numpy as np
     import oracle
     from oracle.numerics import WeightView
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
-    except Exception:
-        cores = os.cpu_count() or 1
+    host = host_description()
+    cores = host["blas_threads"] or os.cpu_count() or 1
     W = WeightView(stored)
     g = w.geom
-    gs = dataclasses.replace(g, n_layers=layers_sample)
-    pos = np.arange(w.seq)
-    t0 = time.perf_counter()
-    hf = oracle.forward(gs, W, tok[0], pos)
-    t1 = time.perf_counter()
-    rows = np.nonzero(oracle.scored_mask(tok, p, w.gen_end, g.mask_id)[0])[0][:rows_sample]
-    oracle.row_stats(oracle.lm_logits(W, hf[rows]))
-    t2 = time.perf_counter()
-    est = (t1 - t0) * g.n_layers / layers_sample + (t2 - t1) * R / len(rows)
-    return {"value": 1.0 / est, "unit": "steps/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"float64 oracle forward over {layers_sample} of {g.n_layers} layers ({t1 - t0:.1f} s) and "
-                      f"LM head + softmax statistics for {len(rows)} of {R} scored rows ({t2 - t1:.1f} s), "
-                      f"scaled to one full step: {est:.1f} s/step",
-            "seconds_per_step": est}
+    kv = None
+    if kv_host is not None:
+        def kv(b, l):
+            import synth
+            k, v = kv_host[l]
+            return synth.bf16_bits_to_f32(k[b]), synth.bf16_bits_to_f32(v[b])
+        kv.prefix = w.kv_prefix
+    if full:
+        t0 = time.perf_counter()
+        oracle.step(g, W, tok, p, w.gen_end, kv=kv)
+        est = time.perf_counter() - t0
+        sample = (f"one full float64 oracle step of the same workload (forward of {tok.shape[0]} x {tok.shape[1]} "
+                  f"tokens over {g.n_layers} layers, statistics of {R} scored rows), measured: {est:.1f} s")
+    else:
+        gs = dataclasses.replace(g, n_layers=layers_sample)
+        pos = w.kv_prefix + np.arange(w.seq)
+        t0 = time.perf_counter()
+        hf = oracle.forward(gs, W, tok[0], pos)
+        t1 = time.perf_counter()
+        rows = np.nonzero(oracle.scored_mask(tok, p, w.gen_end, g.mask_id)[0])[0][:rows_sample]
+        oracle.row_stats(oracle.lm_logits(W, hf[rows]))
+        t2 = time.perf_counter()
+        est = ((t1 - t0) * g.n_layers / layers_sample * tok.shape[0] + (t2 - t1) * R / max(len(rows), 1))
+        sample = (f"float64 oracle forward of one sequence over {layers_sample} of {g.n_layers} layers ({t1 - t0:.1f} s)"
+                  f" and statistics of {len(rows)} of {R} scored rows ({t2 - t1:.1f} s), scaled to one step: "
+                  f"{est:.1f} s")
+    return {"value": 1.0 / est, "unit": "steps/s", "cores": int(cores), "kind": "oracle", "sample": sample,
+            "seconds_per_step": est, "host": host}
 
 
 def main():
@@ -351,8 +391,10 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on a bounded sample (CPU baseline)")
-        cpu = cpu_baseline(w, stored, tok_h, p_h, R)
+        kv_host = [synth.kv_cache_layer(w, l) for l in range(g.n_layers)] if w.kv_prefix else None
+        cpu = cpu_baseline(w, stored, tok_h, p_h, R, kv_host, full=w.key in ("c1", "c2", "c5"))
         cpu = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cpu.items()}
+        del kv_host
         log(f"  {cpu['sample']}")
 
     out = {
