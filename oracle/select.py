@@ -15,7 +15,19 @@ Readings of the paper used here (the paper is silent or inconsistent on them):
 * scored rows (``score_all=False``): x_i = [MASK] and p <= i < gen_end (probabilities
   are defined at masked positions, Section 2.1); only those rows can become drafts.
   ``score_all=True``: every position p <= i < gen_end is scored and may be redrafted.
+* semi-autoregressive blocks (Section 4 setup: semi-AR remasking with blocks of 32; the paper
+  does not say how blocks and the window combine): with ``block_len`` > 0 the generation region is
+  cut into blocks of that length starting at ``block_origin``; the decoding window never crosses
+  the end of the block that holds p (L_eff = min(L, block_end - p), and the re-mask stops there),
+  while drafts keep looking ahead over the whole region from p + L.
 """
+
+
+def block_end(p: int, gen_end: int, block_origin: int, block_len: int) -> int:
+    """End of the semi-AR block holding position p (gen_end without blocks)."""
+    if block_len <= 0:
+        return gen_end
+    return min(gen_end, block_origin + block_len * ((p - block_origin) // block_len + 1))
 import numpy as np
 
 
@@ -38,13 +50,15 @@ def compute_k(conf_window: np.ndarray, tau_commit: float) -> int:
 
 
 def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top1, conf,
-                      no_progress_guard=False, score_all=False, contiguous_drafts=False):
+                      no_progress_guard=False, score_all=False, contiguous_drafts=False,
+                      block_origin=0, block_len=0):
     """One selection step for every sequence: steps (iii)-(iv) of Section 3.3, then (i) for the next.
 
     tokens [B,S], p [B], top1/conf [B,S] (statistics of the forward on ``tokens``).
     Returns (new tokens, new p, K_raw [B], K_eff [B]); inputs are not modified.
     Per sequence with p < gen_end:
-      L_eff = min(L, gen_end - p); K = Eq. compute_k over conf[p : p + L_eff];
+      L_eff = min(L, end - p) with end = gen_end, or the end of p's block with blocks;
+      K = Eq. compute_k over conf[p : p + L_eff];
       K_eff = max(K, 1) (unless no_progress_guard, or the row at p has no prediction: top1 = -1);
       commit x[p : p + K_eff] = top1                                 (Algorithm 1, commit)
       for j in [p + L, gen_end): if (x_j = [MASK] or score_all) and conf_j > tau_draft:
@@ -53,7 +67,7 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
         is drafted: it ends at the first eligible position with conf <= tau_draft; positions
         that already hold a token (not eligible) keep it and do not end the chain
       p += K_eff                                                     (Algorithm 1, advance)
-      x[p : min(p + L, gen_end)] = [MASK]                            (Eq. remasking, next iteration)
+      x[p : min(p + L, end of the new p's block)] = [MASK]           (Eq. remasking, next iteration)
     """
     x = np.array(tokens, dtype=np.int64, copy=True)
     pn = np.array(p, dtype=np.int64, copy=True)
@@ -64,7 +78,7 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
         pb = int(pn[b])
         if pb >= gen_end:
             continue
-        L_eff = min(L, gen_end - pb)
+        L_eff = min(L, block_end(pb, gen_end, block_origin, block_len) - pb)
         K = compute_k(conf[b, pb:pb + L_eff], tau_commit)
         has_prediction = top1[b, pb] >= 0
         Ke = K if (no_progress_guard or not has_prediction) else max(K, 1)
@@ -79,7 +93,7 @@ def select_contiguous(tokens, p, gen_end, L, tau_commit, tau_draft, mask_id, top
                 break                                     # the chain of Appendix E ends here
         pb += Ke
         pn[b] = pb
-        for j in range(pb, min(pb + L, gen_end)):
+        for j in range(pb, min(pb + L, block_end(pb, gen_end, block_origin, block_len))):
             x[b, j] = mask_id
     return x, pn, K_raw, K_eff
 

@@ -92,3 +92,61 @@ def test_drafts_written_and_later_invalidated(tiny_weights):
             if (xt[b, pt[b] + L:] != mask).any():
                 saw_draft = True
     assert saw_draft
+
+
+# ---------------------------------------------------------------- semi-autoregressive blocks (reading R24)
+
+def test_block_end_tiles_the_generation_region():
+    from oracle.select import block_end
+    assert [block_end(p, 100, 32, 16) for p in (32, 40, 47, 48, 95, 96, 99)] == [48, 48, 48, 64, 96, 100, 100]
+    assert block_end(50, 100, 32, 0) == 100                      # no blocks: the generation end
+    assert block_end(31, 100, 32, 16) == 32                      # before the origin: the origin
+
+
+def test_one_block_covering_the_region_is_no_blocking(tiny_weights):
+    w, W, prompt = _setup(tiny_weights)
+    M, L = 24, 8
+    a, sa = generate(w.geom, W, prompt, M, L, 0.7, 0.9)
+    b, sb = generate(w.geom, W, prompt, M, L, 0.7, 0.9, block_len=M)
+    np.testing.assert_array_equal(a, b)
+    assert sa == sb
+
+
+def test_blocks_of_one_token_are_sequential_greedy(tiny_weights):
+    """Blocks of length 1 clip every window to one position: with drafts off each iteration commits the
+    top-1 at p, i.e. chain-rule greedy decoding (Section 2.2), whatever tau_commit is."""
+    w, W, prompt = _setup(tiny_weights)
+    M = 10
+    x, steps = generate(w.geom, W, prompt, M, 8, 0.0, 1.01, block_len=1)
+    assert steps == M
+    np.testing.assert_array_equal(x, sequential_greedy(w.geom, W, prompt, M))
+
+
+def test_window_never_crosses_a_block_end(tiny_weights):
+    """With blocks of 8 and a window of 16: each iteration commits inside the block holding p, p lands
+    on every block end (no block is skipped), the re-masked window stops at the block end, and drafts
+    past p + L are still written."""
+    w, W, prompt = _setup(tiny_weights)
+    M, L, BL = 32, 16, 8
+    N = prompt.shape[1]
+    trace = []
+    generate(w.geom, W, prompt, M, L, 0.2, 0.5, trace=trace, block_len=BL)
+    mask = w.geom.mask_id
+    prev_p = np.full(prompt.shape[0], N)
+    visited = [set([N]) for _ in range(prompt.shape[0])]
+    saw_draft = False
+    for xt, pt, kr, ke in trace:
+        for b in range(prompt.shape[0]):
+            if prev_p[b] >= N + M:
+                continue
+            be = N + BL * ((prev_p[b] - N) // BL + 1)
+            assert pt[b] <= be                                   # the commit stayed in the block
+            visited[b].add(int(pt[b]))
+            nbe = min(N + M, N + BL * ((pt[b] - N) // BL + 1))
+            assert (xt[b, pt[b]:nbe] == mask).all()
+            if pt[b] + L < N + M and (xt[b, pt[b] + L:] != mask).any():
+                saw_draft = True
+        prev_p = pt
+    for b in range(prompt.shape[0]):
+        assert {N + k * BL for k in range(M // BL + 1)} <= visited[b]
+    assert saw_draft

@@ -85,7 +85,8 @@ def test_golden_select_cases(case):
     tok = np.array([case["tokens"]])
     x, p, kr, ke = select_contiguous(tok, np.array([case["p"]]), case["gen_end"], case["L"],
                                      case["tau_commit"], case["tau_draft"], case["mask_id"],
-                                     np.array([case["top1"]]), np.array([case["conf"]]))
+                                     np.array([case["top1"]]), np.array([case["conf"]]),
+                                     block_origin=case.get("block_origin", 0), block_len=case.get("block_len", 0))
     assert x[0].tolist() == case["expect_tokens"]
     assert (p[0], kr[0], ke[0]) == (case["expect_p"], case["expect_K_raw"], case["expect_K_eff"])
 
