@@ -84,7 +84,9 @@ typedef struct {
  * v[l] -> bf16 [B, n_kv_heads, head_dim, capacity] values (key index contiguous); positions
  * [0, prefix_len) are in use. capacity = 0 means capacity = prefix_len.
  * `k` and `v` themselves are HOST arrays of n_layers device pointers (writable buffers for
- * dcl_kv_append). prefix_len % 8 == 0, capacity % 8 == 0, prefix_len <= capacity. */
+ * dcl_kv_append). prefix_len >= 0, capacity % 8 == 0, prefix_len <= capacity. A prefix length that is not
+ * a multiple of 8 (for example after appending the K_eff tokens one iteration committed) is supported:
+ * the step carries the last prefix_len % 8 cached keys and values next to its fresh ones. */
 typedef struct {
   const void* const* k;
   const void* const* v;
@@ -150,7 +152,8 @@ size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_p
  * S tokens alone, otherwise they also attend to the cached prefix. Token ids outside
  * [0, vocab) read an all-zero embedding row. Writes `out` (all B*S rows). ws: device,
  * ws_bytes >= dcl_workspace_bytes(model, B, S, prefix), 256-byte aligned. Sizes: B*S <= 2^22
- * (DCL_E_ARG otherwise), B*(S+8)*(n_heads + 2*n_kv_heads)*head_dim < 2^31 and
+ * (DCL_E_ARG otherwise), B*(S+8)*(n_heads + 2*n_kv_heads)*head_dim < 2^31 (S+16 with a prefix length
+ * that is not a multiple of 8) and
  * B*S*max(d_model, n_heads*head_dim, d_ffn) < 2^31 (DCL_E_UNSUPPORTED otherwise: the kernels
  * address q/k/v^T and the GEMM operands with 32-bit offsets). */
 dcl_status dcl_denoise_step(dcl_model_t model, const int32_t* tokens, int32_t B, int32_t S,
@@ -175,15 +178,20 @@ dcl_status dcl_denoise_step_noalloc(dcl_model_t model, const int32_t* tokens, in
 
 /* Steps (iii), (iv) and (i) for every sequence b with p[b] < gen_end, in place on tokens [B, S]
  * and p [B] (device), using statistics `in` of a dcl_denoise_step on the same tokens:
- *   L_eff = min(L, gen_end - p);  K = number of leading window rows with conf > tau_commit
+ *   end(q) = gen_end, or with semi-autoregressive blocks (block_len > 0; Section 4 setup, blocks of 32)
+ *   the end of the block holding position q, blocks of block_len positions tiling the line from
+ *   block_origin (normally the prompt length), capped at gen_end;
+ *   L_eff = min(L, end(p) - p);  K = number of leading window rows with conf > tau_commit
  *   (Eq. compute_k);  K_eff = max(K, 1) unless DCL_SEL_NO_PROGRESS_GUARD (K = 0 would stall
  *   Algorithm 1; committing the top-1 at p is one sequential step);  x[p, p+K_eff) = top1;
  *   for j in [p+L, gen_end) with x[j] == mask_id (any x[j] with DCL_SEL_SCORE_ALL) and
  *   conf[j] > tau_draft: x[j] = top1[j] (Eq. draft_update);  p += K_eff;
- *   x[p, min(p+L, gen_end)) = mask_id (Eq. remasking for the next iteration).
+ *   x[p, min(p+L, end(p))) = mask_id with the new p (Eq. remasking for the next iteration).
+ * The window thus never crosses a block end, while drafts still look ahead over [p+L, gen_end).
  * A window start whose row was not scored (top1 < 0) is never committed. Sequences with
  * p >= gen_end (or p < 0) are untouched (K_raw = K_eff = 0). K_raw, K_eff: device [B] outputs (may be
- * NULL). 1 <= L; 0 <= tau_commit <= 1; tau_draft >= 0 (values > 1 disable drafts).
+ * NULL). 1 <= L; block_len >= 0 (0: no blocks); with blocks 0 <= block_origin <= S; 0 <= tau_commit <= 1;
+ * tau_draft >= 0 (values > 1 disable drafts).
  * DCL_SEL_CONTIGUOUS_DRAFTS (the variant of Appendix E): only the leading chain of the draft
  *   region is drafted; it ends at the first eligible position (as above) with conf <= tau_draft,
  *   and positions that already hold a token keep it without ending the chain.
@@ -194,13 +202,14 @@ dcl_status dcl_denoise_step_noalloc(dcl_model_t model, const int32_t* tokens, in
  *   drafts and no remasking. K_raw = number above tau_commit, K_eff = number committed.
  * DCL_SEL_MARGIN: every comparison above uses conf - p2 (float32) in place of conf. */
 dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end,
-                                 int32_t L, float tau_commit, float tau_draft, int32_t mask_id,
-                                 dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,
-                                 hipStream_t stream);
+                                 int32_t L, int32_t block_origin, int32_t block_len, float tau_commit,
+                                 float tau_draft, int32_t mask_id, dcl_row_stats in, int32_t* K_raw,
+                                 int32_t* K_eff, uint32_t flags, hipStream_t stream);
 
 /* Algorithm 1 (Section 3, Appendix A) end to end on the device: Eq. remasking of the first window,
  * then repeated iterations of dcl_denoise_step (flags `score_flags`) followed by
- * dcl_select_contiguous (tau_commit, tau_draft, `select_flags`, mask_id of the model), until every
+ * dcl_select_contiguous (L, block_origin, block_len, tau_commit, tau_draft, `select_flags`, mask_id of
+ * the model; block_len > 0 gives the semi-autoregressive block decoding of Section 4), until every
  * sequence has p >= gen_end or max_steps iterations ran. tokens [B, S] and p [B] (device) hold the
  * state in and out; stats, K_raw, K_eff and ws are as for the two calls above (K_raw, K_eff may be
  * NULL). k_hist (device int32 [L + 1], may be NULL) is incremented at K_eff once per sequence and
@@ -217,7 +226,8 @@ dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t*
  * 1 <= max_steps, 1 <= check_every; other argument rules as for the two calls. */
 dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S, int32_t* p,
                         int32_t gen_end, const dcl_kv* kv, uint32_t score_flags, int32_t L,
-                        float tau_commit, float tau_draft, uint32_t select_flags, int32_t max_steps,
+                        int32_t block_origin, int32_t block_len, float tau_commit, float tau_draft,
+                        uint32_t select_flags, int32_t max_steps,
                         int32_t check_every, dcl_row_stats stats, int32_t* K_raw, int32_t* K_eff,
                         int32_t* k_hist, void* ws, size_t ws_bytes, int32_t* steps_out,
                         hipStream_t stream);
@@ -255,12 +265,14 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
                             void* hidden_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Test support: the intermediate tensors of one transformer layer, each a device buffer of the stated
- * layout or NULL (not written). T = B*S, Sp = S rounded up to a multiple of 8. */
+ * layout or NULL (not written). T = B*S. */
 typedef struct {
   void* u;       /* bf16 [T, d_model]: bf16(RMSNorm(r_in) * g_attn) */
   void* q;       /* bf16 [B, n_heads, S, head_dim]: queries after bias and RoPE */
-  void* k;       /* bf16 [B, n_kv_heads, S, head_dim]: keys after bias and RoPE */
-  void* v;       /* bf16 [B, n_kv_heads, head_dim, Sp]: values, key index contiguous (keys >= S are 0) */
+  void* k;       /* bf16 [B, n_kv_heads, c + S, head_dim]: keys after bias and RoPE, token s in slot c + s,
+                    where c = prefix_len % 8 (slots [0, c) hold the newest cached keys) */
+  void* v;       /* bf16 [B, n_kv_heads, head_dim, Sp]: values, key index contiguous in the same slots,
+                    Sp = c + S rounded up to 8 (slots >= c + S are 0) */
   void* o;       /* bf16 [T, n_heads * head_dim]: attention output (softmax(q k^T / sqrt(dh)) v, no mask) */
   float* r_mid;  /* [T, d_model]: r_in + o W_o^T */
   void* u2;      /* bf16 [T, d_model]: bf16(RMSNorm(r_mid) * g_ffn) */

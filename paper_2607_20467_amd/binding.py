@@ -91,10 +91,10 @@ def load_library():
                                             vp, sz, vp]),
         "dcl_denoise_step_noalloc": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32,
                                                     DclRowStats, vp]),
-        "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, f32, f32, i32, DclRowStats, vp, vp,
-                                                 u32, vp]),
-        "dcl_generate": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, i32, f32, f32, u32,
-                                        i32, i32, DclRowStats, vp, vp, vp, vp, sz, ctypes.POINTER(i32), vp]),
+        "dcl_select_contiguous": (ctypes.c_int, [vp, i32, i32, vp, i32, i32, i32, i32, f32, f32, i32, DclRowStats,
+                                                 vp, vp, u32, vp]),
+        "dcl_generate": (ctypes.c_int, [vp, vp, i32, i32, vp, i32, ctypes.POINTER(DclKV), u32, i32, i32, i32, f32, f32,
+                                        u32, i32, i32, DclRowStats, vp, vp, vp, vp, sz, ctypes.POINTER(i32), vp]),
         "dcl_score_workspace_bytes": (sz, [vp, i32]),
         "dcl_kv_append": (ctypes.c_int, [vp, vp, i32, i32, ctypes.POINTER(DclKV), vp, sz, vp]),
         "dcl_profile_enable": (ctypes.c_int, [i32]),
@@ -260,23 +260,28 @@ def dcl_denoise_step_noalloc(model: int, tokens, B: int, S: int, p, gen_end: int
 
 
 def dcl_select_contiguous(tokens, B: int, S: int, p, gen_end: int, L: int, tau_commit: float, tau_draft: float,
-                          mask_id: int, stats, k_raw=None, k_eff=None, flags: int = 0, stream=None) -> None:
+                          mask_id: int, stats, k_raw=None, k_eff=None, flags: int = 0, stream=None,
+                          block_origin: int = 0, block_len: int = 0) -> None:
+    """block_origin / block_len: semi-autoregressive blocks (block_len 0 = none), as in include/dcl.h."""
     w = "dcl_select_contiguous"
     tp, pp = _state(tokens, p, B, S, w)
-    _check(load_library().dcl_select_contiguous(tp, B, S, pp, gen_end, L, tau_commit, tau_draft, mask_id,
+    _check(load_library().dcl_select_contiguous(tp, B, S, pp, gen_end, L, block_origin, block_len, tau_commit,
+                                                tau_draft, mask_id,
                                                 _stats(stats, B * S, w), _arg(k_raw, "k_raw", w, _I32, B),
                                                 _arg(k_eff, "k_eff", w, _I32, B), flags, _stream(stream)), w)
 
 
 def dcl_generate(model: int, tokens, B: int, S: int, p, gen_end: int, kv, score_flags: int, L: int,
                  tau_commit: float, tau_draft: float, select_flags: int, max_steps: int, check_every: int, stats,
-                 k_raw, k_eff, k_hist, ws, ws_bytes: int, stream=None) -> int:
-    """Returns the number of iterations run."""
+                 k_raw, k_eff, k_hist, ws, ws_bytes: int, stream=None, block_origin: int = 0,
+                 block_len: int = 0) -> int:
+    """Returns the number of iterations run. block_origin / block_len: semi-autoregressive blocks."""
     w = "dcl_generate"
     kvp, keep = _kv(kv, model, B, w)
     tp, pp = _state(tokens, p, B, S, w)
     steps = ctypes.c_int32(0)
-    _check(load_library().dcl_generate(model, tp, B, S, pp, gen_end, kvp, score_flags, L, tau_commit,
+    _check(load_library().dcl_generate(model, tp, B, S, pp, gen_end, kvp, score_flags, L, block_origin, block_len,
+                                       tau_commit,
                                        tau_draft, select_flags, max_steps, check_every, _stats(stats, B * S, w),
                                        _arg(k_raw, "k_raw", w, _I32, B), _arg(k_eff, "k_eff", w, _I32, B),
                                        _arg(k_hist, "k_hist", w, _I32, L + 1 if L >= 0 else None),
@@ -335,11 +340,13 @@ def dcl_debug_layer(model: int, B: int, S: int, kv, layer: int, r_in, taps: dict
     """taps: dict name -> device tensor (names of DclLayerTaps; absent = not copied out)."""
     w = "dcl_debug_layer"
     g = _cfg_of(model)
-    T, Sp = B * S, (S + 7) // 8 * 8
+    koff = (kv[2] % 8) if kv is not None else 0      # carried cached keys in front of the fresh ones
+    T, Sp = B * S, (koff + S + 7) // 8 * 8
     size = {}
     if g is not None:
         hd, kd = g.n_heads * g.head_dim, g.n_kv_heads * g.head_dim
-        size = {"u": (_B16, T * g.d_model), "q": (_B16, T * hd), "k": (_B16, T * kd), "v": (_B16, B * kd * Sp),
+        size = {"u": (_B16, T * g.d_model), "q": (_B16, T * hd), "k": (_B16, B * (koff + S) * kd),
+                "v": (_B16, B * kd * Sp),
                 "o": (_B16, T * hd), "r_mid": (_F32, T * g.d_model), "u2": (_B16, T * g.d_model),
                 "a": (_B16, T * g.d_ffn), "r_out": (_F32, T * g.d_model)}
     unknown = set(taps) - {f for f, _ in DclLayerTaps._fields_}

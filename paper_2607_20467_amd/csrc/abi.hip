@@ -90,7 +90,7 @@ WeightLayout make_layout(const dcl_config& c) {
   return L;
 }
 
-StepLayout step_layout(const dcl_config& c, int B, int S) {
+StepLayout step_layout(const dcl_config& c, int B, int S, int P) {
   StepLayout L;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -101,12 +101,14 @@ StepLayout step_layout(const dcl_config& c, int B, int S) {
   const size_t T = (size_t)B * S, d = c.d_model, dh = c.head_dim;
   L.T = (int)T;
   L.S = S;
-  L.Sp = (S + 7) / 8 * 8;
+  L.koff = P > 0 ? P % 8 : 0;
+  L.Sk = L.koff + S;
+  L.Sp = (L.Sk + 7) / 8 * 8;
   L.n_vt = (c.vocab + kLmTile - 1) / kLmTile;
   L.r = take(T * d * 4);
   L.u = take(T * d * 2);
   L.q = take(T * c.n_heads * dh * 2);
-  L.k = take(T * c.n_kv_heads * dh * 2);
+  L.k = take((size_t)B * L.Sk * c.n_kv_heads * dh * 2);
   L.vt = take((size_t)B * c.n_kv_heads * dh * L.Sp * 2);
   L.o = take(T * c.n_heads * dh * 2);
   L.a = take(T * c.d_ffn * 2);
@@ -197,7 +199,10 @@ dcl_status check_shape_args(const Model* m, int32_t B, int32_t S, const dcl_kv* 
   if (!m) return fail(DCL_E_ARG, "model is NULL");
   if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
   if ((long)B * S > (1 << 22)) return fail(DCL_E_ARG, "B*S = %ld too large", (long)B * S);
-  if ((long)B * (S + 8) * m->qkv_rows() >= (1L << 31))  // the QKV epilogue addresses q/k/v^T with 32 bits
+  // the QKV epilogue addresses q/k/v^T with 32 bits; a ragged cached prefix adds up to 7 carried keys (and
+  // their padding) per sequence
+  const int pad = (kv && kv->prefix_len % 8 != 0) ? 16 : 8;
+  if ((long)B * (S + pad) * m->qkv_rows() >= (1L << 31))
     return fail(DCL_E_UNSUPPORTED, "B*S = %ld tokens: q/k/v would reach 2^31 elements", (long)B * S);
   // the GEMMs address their activation operand ([tokens, K], K up to max(d_model, H*dh, d_ffn)) with 32 bits
   const long kmax = std::max({(long)m->cfg.d_model, (long)m->cfg.n_heads * m->cfg.head_dim, (long)m->cfg.d_ffn});
@@ -207,7 +212,7 @@ dcl_status check_shape_args(const Model* m, int32_t B, int32_t S, const dcl_kv* 
   const int P = kv ? kv->prefix_len : 0;
   if (kv) {
     if (!kv->k || !kv->v) return fail(DCL_E_ARG, "kv->k / kv->v is NULL");
-    if (P < 0 || P % 8 != 0) return fail(DCL_E_UNSUPPORTED, "kv prefix_len %d must be a non-negative multiple of 8", P);
+    if (P < 0) return fail(DCL_E_ARG, "kv prefix_len %d must be >= 0", P);
     const int cap = kv->capacity ? kv->capacity : P;
     if (cap < P || cap % 8 != 0)
       return fail(DCL_E_ARG, "kv capacity %d must be a multiple of 8 and >= prefix_len %d", kv->capacity, P);
@@ -219,10 +224,10 @@ dcl_status check_shape_args(const Model* m, int32_t B, int32_t S, const dcl_kv* 
   return DCL_OK;
 }
 
-dcl_status check_workspace(const Model* m, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
+dcl_status check_workspace(const Model* m, int32_t B, int32_t S, int32_t P, void* ws, size_t ws_bytes) {
   if (!ws) return fail(DCL_E_ARG, "workspace is NULL");
   if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(DCL_E_ARG, "workspace must be 256-byte aligned");
-  const size_t need = step_layout(m->cfg, B, S).total;
+  const size_t need = step_layout(m->cfg, B, S, P).total;
   if (ws_bytes < need) return fail(DCL_E_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
   return DCL_OK;
 }
@@ -233,7 +238,7 @@ dcl_status check_step_args(const Model* m, const int32_t* tokens, int32_t B, int
   if (st != DCL_OK) return st;
   if (!tokens) return fail(DCL_E_ARG, "tokens is NULL");
   if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
-  return check_workspace(m, B, S, ws, ws_bytes);
+  return check_workspace(m, B, S, kv ? kv->prefix_len : 0, ws, ws_bytes);
 }
 
 // Device-to-device copy of a stage's result into a caller buffer (test support; null = not wanted).
@@ -274,28 +279,34 @@ int run_layer(const Model* m, int l, int B, int S, const dcl_kv* kv, void* ws, c
   qo.dh = dh;
   qo.S = S;
   qo.Sp = L.Sp;
+  qo.Sk = L.Sk;
+  qo.koff = L.koff;
   qo.pos0 = P;
   {
     PROF(P_QKV);
     gemm_qkv(at<bf16_t>(wb, lo.wqkv), u, m->qkv_rows(), T, d, qo, s);
   }
+  const int Pc = kv ? (kv->capacity ? kv->capacity : P) : 0;
+  if (kv && L.koff > 0)  // the newest P mod 8 cached keys/values in front of the fresh ones
+    launch_kv_carry(static_cast<const bf16_t*>(kv->k[l]), static_cast<const bf16_t*>(kv->v[l]), qo.k, qo.vt, B,
+                    c.n_kv_heads, L.Sk, L.Sp, dh, P, Pc, s);
   if (taps) {
     tap(taps->q, qo.q, (size_t)T * c.n_heads * dh * 2, s);
-    tap(taps->k, qo.k, (size_t)T * c.n_kv_heads * dh * 2, s);
+    tap(taps->k, qo.k, (size_t)B * L.Sk * c.n_kv_heads * dh * 2, s);
     tap(taps->v, qo.vt, (size_t)B * c.n_kv_heads * dh * L.Sp * 2, s);
   }
   if (writeback) {  // this layer's fresh keys and values into the cache at [P, P + S)
     launch_kv_writeback(qo.k, qo.vt, static_cast<bf16_t*>(const_cast<void*>(kv->k[l])),
-                        static_cast<bf16_t*>(const_cast<void*>(kv->v[l])), B, c.n_kv_heads, S, L.Sp, dh, P,
-                        kv->capacity ? kv->capacity : P, s);
+                        static_cast<bf16_t*>(const_cast<void*>(kv->v[l])), B, c.n_kv_heads, S, L.Sk, L.Sp, L.koff,
+                        dh, P, Pc, s);
     if (l == c.n_layers - 1) return -1;  // nothing after the last layer's keys and values is needed
   }
   AttnArgs aa;
   aa.q = qo.q;
   aa.k = qo.k;
   aa.vt = qo.vt;
-  aa.kc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->k[l]) : nullptr;
-  aa.vc = (kv && P > 0) ? static_cast<const bf16_t*>(kv->v[l]) : nullptr;
+  aa.kc = (kv && P - L.koff > 0) ? static_cast<const bf16_t*>(kv->k[l]) : nullptr;
+  aa.vc = (kv && P - L.koff > 0) ? static_cast<const bf16_t*>(kv->v[l]) : nullptr;
   aa.o = o;
   aa.B = B;
   aa.H = c.n_heads;
@@ -303,8 +314,9 @@ int run_layer(const Model* m, int l, int B, int S, const dcl_kv* kv, void* ws, c
   aa.dh = dh;
   aa.S = S;
   aa.Sp = L.Sp;
-  aa.P = P;
-  aa.Pc = kv ? (kv->capacity ? kv->capacity : P) : 0;
+  aa.Sk = L.Sk;
+  aa.P = P - L.koff;  // whole 8-key chunks of the cache; the rest was carried into the fresh buffers
+  aa.Pc = Pc;
   aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
   {
     PROF(P_ATTN);
@@ -378,7 +390,7 @@ dcl_status check_denoise_args(const Model* m, const int32_t* tokens, int32_t B, 
 void enqueue_denoise(const Model* m, const int32_t* tokens, int32_t B, int32_t S, const int32_t* p, int32_t gen_end,
                      const dcl_kv* kv, uint32_t flags, const dcl_row_stats& out, void* ws, hipStream_t stream) {
   const dcl_config& c = m->cfg;
-  const StepLayout L = step_layout(c, B, S);
+  const StepLayout L = step_layout(c, B, S, kv ? kv->prefix_len : 0);
   const int pending = run_forward(m, tokens, B, S, kv, ws, L, stream);
   int32_t* rows = at<int32_t>(ws, L.rows);
   int32_t* count = at<int32_t>(ws, L.count);
@@ -415,13 +427,17 @@ void enqueue_denoise(const Model* m, const int32_t* tokens, int32_t B, int32_t S
 }
 
 dcl_status check_select_args(const int32_t* tokens, int32_t B, int32_t S, const int32_t* p, int32_t gen_end,
-                             int32_t L, float tau_commit, float tau_draft, const dcl_row_stats& in, uint32_t flags) {
+                             int32_t L, int32_t block_origin, int32_t block_len, float tau_commit, float tau_draft,
+                             const dcl_row_stats& in, uint32_t flags) {
   if (!tokens || !p) return fail(DCL_E_ARG, "tokens / p is NULL");
   if (!in.top1 || !in.conf) return fail(DCL_E_ARG, "in.top1 / in.conf is NULL");
   if ((flags & DCL_SEL_MARGIN) && !in.p2) return fail(DCL_E_ARG, "DCL_SEL_MARGIN needs in.p2");
   if (B < 1 || S < 1) return fail(DCL_E_ARG, "B=%d, S=%d must be >= 1", B, S);
   if (gen_end < 0 || gen_end > S) return fail(DCL_E_ARG, "gen_end %d outside [0, S=%d]", gen_end, S);
   if (L < 1) return fail(DCL_E_ARG, "window L=%d must be >= 1", L);
+  if (block_len < 0) return fail(DCL_E_ARG, "block_len %d must be >= 0", block_len);
+  if (block_len > 0 && (block_origin < 0 || block_origin > S))
+    return fail(DCL_E_ARG, "block_origin %d outside [0, S=%d]", block_origin, S);
   if (!(tau_commit >= 0.f && tau_commit <= 1.f)) return fail(DCL_E_ARG, "tau_commit %g outside [0, 1]", tau_commit);
   if (!(tau_draft >= 0.f) || isnan(tau_draft)) return fail(DCL_E_ARG, "tau_draft %g must be >= 0", tau_draft);
   if (flags & ~(uint32_t)(DCL_SEL_NO_PROGRESS_GUARD | DCL_SEL_SCORE_ALL | DCL_SEL_NONCONTIGUOUS |
@@ -589,7 +605,7 @@ dcl_status dcl_load_weights(dcl_model_t model, void* dev_buf, size_t bytes, cons
 size_t dcl_workspace_bytes(dcl_model_t model, int32_t B, int32_t S, int32_t kv_prefix) {
   Model* m = reinterpret_cast<Model*>(model);
   if (!m || B < 1 || S < 1 || kv_prefix < 0 || (long)B * S > (1 << 22)) return 0;
-  return step_layout(m->cfg, B, S).total;
+  return step_layout(m->cfg, B, S, kv_prefix).total;
 }
 
 
@@ -609,7 +625,7 @@ dcl_status dcl_denoise_step_noalloc(dcl_model_t model, const int32_t* tokens, in
   Model* m = reinterpret_cast<Model*>(model);
   dcl_status st = check_shape_args(m, B, S, kv);
   if (st != DCL_OK) return st;
-  const size_t need = step_layout(m->cfg, B, S).total;
+  const size_t need = step_layout(m->cfg, B, S, kv ? kv->prefix_len : 0).total;
   if (need > (size_t)DCL_NOALLOC_SCRATCH_BYTES)
     return fail(DCL_E_WORKSPACE, "B=%d, S=%d needs %zu bytes of scratch; the static scratch holds %zu (use "
                 "dcl_denoise_step with a workspace)", B, S, need, (size_t)DCL_NOALLOC_SCRATCH_BYTES);
@@ -625,28 +641,32 @@ dcl_status dcl_denoise_step_noalloc(dcl_model_t model, const int32_t* tokens, in
 }
 
 dcl_status dcl_select_contiguous(int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end, int32_t L,
-                                 float tau_commit, float tau_draft, int32_t mask_id, dcl_row_stats in,
-                                 int32_t* K_raw, int32_t* K_eff, uint32_t flags, hipStream_t stream) {
-  dcl_status st = check_select_args(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, in, flags);
+                                 int32_t block_origin, int32_t block_len, float tau_commit, float tau_draft,
+                                 int32_t mask_id, dcl_row_stats in, int32_t* K_raw, int32_t* K_eff, uint32_t flags,
+                                 hipStream_t stream) {
+  dcl_status st = check_select_args(tokens, B, S, p, gen_end, L, block_origin, block_len, tau_commit, tau_draft, in,
+                                    flags);
   if (st != DCL_OK) return st;
   (void)hipGetLastError();
   {
     hipStream_t s = stream;
     PROF(P_SELECT);
-    launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, in, K_raw, K_eff, flags, stream);
+    launch_select(tokens, B, S, p, gen_end, L, block_origin, block_len, tau_commit, tau_draft, mask_id, in, K_raw,
+                  K_eff, flags, stream);
   }
   return hip_check(hipGetLastError(), "select launch");
 }
 
 dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S, int32_t* p, int32_t gen_end,
-                        const dcl_kv* kv, uint32_t score_flags, int32_t L, float tau_commit, float tau_draft,
-                        uint32_t select_flags, int32_t max_steps, int32_t check_every, dcl_row_stats stats,
-                        int32_t* K_raw, int32_t* K_eff, int32_t* k_hist, void* ws, size_t ws_bytes,
-                        int32_t* steps_out, hipStream_t stream) {
+                        const dcl_kv* kv, uint32_t score_flags, int32_t L, int32_t block_origin,
+                        int32_t block_len, float tau_commit, float tau_draft, uint32_t select_flags, int32_t max_steps,
+                        int32_t check_every, dcl_row_stats stats, int32_t* K_raw, int32_t* K_eff, int32_t* k_hist,
+                        void* ws, size_t ws_bytes, int32_t* steps_out, hipStream_t stream) {
   Model* m = reinterpret_cast<Model*>(model);
   dcl_status st = check_denoise_args(m, tokens, B, S, p, gen_end, kv, score_flags, stats, ws, ws_bytes);
   if (st != DCL_OK) return st;
-  st = check_select_args(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, stats, select_flags);
+  st = check_select_args(tokens, B, S, p, gen_end, L, block_origin, block_len, tau_commit, tau_draft, stats,
+                         select_flags);
   if (st != DCL_OK) return st;
   if (max_steps < 1 || check_every < 1) return fail(DCL_E_ARG, "max_steps %d and check_every %d must be >= 1",
                                                     max_steps, check_every);
@@ -668,8 +688,8 @@ dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S
     enqueue_denoise(m, tokens, B, S, p, gen_end, kv, score_flags, stats, ws, q);
     hipStream_t s = q;
     PROF(P_SELECT);
-    launch_select(tokens, B, S, p, gen_end, L, tau_commit, tau_draft, mask_id, stats, K_raw, K_eff, select_flags, q,
-                  k_hist);
+    launch_select(tokens, B, S, p, gen_end, L, block_origin, block_len, tau_commit, tau_draft, mask_id, stats, K_raw,
+                  K_eff, select_flags, q, k_hist);
   };
   auto check = [&]() -> dcl_status {  // host copy of p: done when every sequence reached gen_end
     dcl_status e = hip_check(hipMemcpyAsync(ph.data(), p, (size_t)B * sizeof(int32_t), hipMemcpyDeviceToHost, gs),
@@ -686,7 +706,7 @@ dcl_status dcl_generate(dcl_model_t model, int32_t* tokens, int32_t B, int32_t S
   if (st == DCL_OK) st = hip_check(hipStreamWaitEvent(gs, ev, 0), "hipStreamWaitEvent");
   if (st == DCL_OK) {
     // Algorithm 1's loop-top draft invalidation for the first iteration; later ones end with it
-    launch_remask(tokens, B, S, p, gen_end, L, mask_id, gs);
+    launch_remask(tokens, B, S, p, gen_end, L, block_origin, block_len, mask_id, gs);
     st = check();
   }
   // The first iteration runs eagerly (it also performs every one-time kernel set-up, which must not
@@ -737,7 +757,7 @@ dcl_status dcl_kv_append(dcl_model_t model, const int32_t* tokens, int32_t B, in
   if ((long)kv->prefix_len + S > cap)
     return fail(DCL_E_ARG, "prefix_len %d + S %d exceeds the cache capacity %d", kv->prefix_len, S, cap);
   (void)hipGetLastError();
-  run_forward(m, tokens, B, S, kv, ws, step_layout(m->cfg, B, S), stream, true);
+  run_forward(m, tokens, B, S, kv, ws, step_layout(m->cfg, B, S, kv->prefix_len), stream, true);
   return hip_check(hipGetLastError(), "kv_append launch");
 }
 
@@ -825,7 +845,7 @@ dcl_status dcl_debug_logits(dcl_model_t model, const int32_t* tokens, int32_t B,
   if (!rows || !out) return fail(DCL_E_ARG, "rows / out is NULL");
   if (n_rows < 1 || n_rows > B * S) return fail(DCL_E_ARG, "n_rows %d outside [1, B*S]", n_rows);
   const dcl_config& c = m->cfg;
-  const StepLayout L = step_layout(c, B, S);
+  const StepLayout L = step_layout(c, B, S, kv ? kv->prefix_len : 0);
   (void)hipGetLastError();
   const int pending = run_forward(m, tokens, B, S, kv, ws, L, stream);
   // the row count goes to the device through a kernel argument (no host buffer to keep alive)
@@ -851,9 +871,9 @@ dcl_status dcl_debug_layer(dcl_model_t model, int32_t B, int32_t S, const dcl_kv
   if (layer < 0 || layer >= m->cfg.n_layers) return fail(DCL_E_ARG, "layer %d outside [0, %d)", layer, m->cfg.n_layers);
   if (!r_in) return fail(DCL_E_ARG, "r_in is NULL");
   if (!m->loaded) return fail(DCL_E_STATE, "weights not loaded");
-  st = check_workspace(m, B, S, ws, ws_bytes);
+  st = check_workspace(m, B, S, kv ? kv->prefix_len : 0, ws, ws_bytes);
   if (st != DCL_OK) return st;
-  const StepLayout L = step_layout(m->cfg, B, S);
+  const StepLayout L = step_layout(m->cfg, B, S, kv ? kv->prefix_len : 0);
   (void)hipGetLastError();
   st = hip_check(hipMemcpyAsync(at<float>(ws, L.r), r_in, (size_t)B * S * m->cfg.d_model * 4, hipMemcpyDeviceToDevice,
                                 stream), "hipMemcpyAsync(r_in)");

@@ -72,9 +72,12 @@ struct Model {
 };
 
 // Step workspace layout.
+// Fresh keys/values of a step: with a cached prefix of P positions the P mod 8 newest cached keys are
+// carried in front of the S fresh ones (koff = P mod 8), so attention reads the cache only in whole
+// 8-key chunks [0, P - koff); Sk = koff + S keys per (sequence, kv head), Sp = Sk rounded up to 8.
 struct StepLayout {
   size_t r, u, q, k, vt, o, a, rows, count, hf, pm1, pi1, pm2, pi2, ps, pt, part, total;
-  int T, S, Sp, n_vt;
+  int T, S, Sk, Sp, koff, n_vt;
 };
 
 // Vocabulary tile of the fused LM-head reduction (vocab ids per partial) and the number of waves
@@ -94,11 +97,13 @@ void launch_merge(const float* pm1, const int32_t* pi1, const float* pm2, const 
                   const float* ps, const float* pt, int n_vt, const int32_t* rows, const int32_t* count,
                   int max_rows, dcl_row_stats st, hipStream_t s);
 void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s);
-void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c,
-                   float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
+// block_len > 0: semi-AR blocks of block_len positions from block_origin; the window and the re-mask
+// stop at the end of the block holding p.
+void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, int block_origin, int block_len,
+                   float tau_c, float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
                    uint32_t flags, hipStream_t s, int32_t* k_hist = nullptr);
-void launch_remask(int32_t* tokens, int B, int S, const int32_t* p, int gen_end, int L, int mask_id,
-                   hipStream_t s);
+void launch_remask(int32_t* tokens, int B, int S, const int32_t* p, int gen_end, int L, int block_origin,
+                   int block_len, int mask_id, hipStream_t s);
 void launch_pack_rows(const void* src, int src_dtype, bf16_t* dst, int rows, int cols, int mode,
                       int dh, int dst_row0, hipStream_t s);
 void launch_pack_vec(const void* src, int src_dtype, float* dst, int n, int mode, int dh, int dst0,
@@ -110,6 +115,7 @@ struct QkvOut {
   const float* bias;     // packed order, or null
   const float2* rope;    // [max_pos, dh/2] (cos, sin) or null (RoPE off)
   int H, Hkv, dh, S, Sp, pos0;
+  int Sk = 0, koff = 0;  // fresh key rows per (b, kv head) and the slot of token 0 (0, 0: Sk = S)
 };
 struct LmOut {
   float *pm1, *pm2, *ps;
@@ -138,16 +144,21 @@ void gemm_store_f32(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, floa
 
 // Non-causal attention over [cache (P keys) || fresh (S keys)].
 struct AttnArgs {
-  const bf16_t *q, *k, *vt;      // [B,H,S,dh], [B,Hkv,S,dh], [B,Hkv,dh,Sp]
+  const bf16_t *q, *k, *vt;      // [B,H,S,dh] queries; [B,Hkv,Sk,dh], [B,Hkv,dh,Sp] fresh keys / values
   const bf16_t *kc, *vc;         // [B,Hkv,Pc,dh], [B,Hkv,dh,Pc] (first P positions used) or null
   bf16_t* o;                     // [B,S,H*dh]
   int B, H, Hkv, dh, S, Sp, P, Pc;
   float scale_log2;              // log2(e) / sqrt(dh)
+  int Sk = 0;                    // fresh keys per (b, kv head); 0: Sk = S. P must be a multiple of 8.
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
-// Fresh keys k [B,Hkv,S,dh] and values vt [B,Hkv,dh,Sp] into a cache at positions [P, P + S)
-// (kc [B,Hkv,Pc,dh], vc [B,Hkv,dh,Pc]).
-void launch_kv_writeback(const bf16_t* k, const bf16_t* vt, bf16_t* kc, bf16_t* vc, int B, int Hkv, int S, int Sp,
-                         int dh, int P, int Pc, hipStream_t s);
+// The koff = P mod 8 newest cached keys [P - koff, P) and their values into slots [0, koff) of the fresh
+// buffers k [B,Hkv,Sk,dh] and vt [B,Hkv,dh,Sp] (cache kc [B,Hkv,Pc,dh], vc [B,Hkv,dh,Pc]).
+void launch_kv_carry(const bf16_t* kc, const bf16_t* vc, bf16_t* k, bf16_t* vt, int B, int Hkv, int Sk, int Sp,
+                     int dh, int P, int Pc, hipStream_t s);
+// Fresh keys k [B,Hkv,Sk,dh] and values vt [B,Hkv,dh,Sp] of tokens 0..S-1 (slots koff + s) into a cache at
+// positions [P, P + S) (kc [B,Hkv,Pc,dh], vc [B,Hkv,dh,Pc]).
+void launch_kv_writeback(const bf16_t* k, const bf16_t* vt, bf16_t* kc, bf16_t* vc, int B, int Hkv, int S, int Sk,
+                         int Sp, int koff, int dh, int P, int Pc, hipStream_t s);
 
 }  // namespace dcl

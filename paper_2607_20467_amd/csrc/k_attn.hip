@@ -102,7 +102,7 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qw = wid % NQ, kg = wid / NQ;
   const int lq = lane & 15, lg = lane >> 4;
-  const int S = a.S, P = a.P, nkeys = P + S;
+  const int S = a.S, P = a.P, Sk = a.Sk ? a.Sk : a.S, nkeys = P + Sk;  // S queries; P cached + Sk fresh keys
   const int qrow = qt * BQ + qw * 16 + lq;
   const int ntiles = (nkeys + KT - 1) / KT;
   const int nsteps = (ntiles + KG - 1) / KG;
@@ -118,7 +118,7 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   }
   const size_t kvh = (size_t)b * a.Hkv + g;
   const bf16_t* kc = a.kc ? a.kc + kvh * a.Pc * DH : nullptr;
-  const bf16_t* kf = a.k + kvh * S * DH;
+  const bf16_t* kf = a.k + kvh * Sk * DH;
   const bf16_t* vc = a.vc ? a.vc + kvh * DH * a.Pc : nullptr;
   const bf16_t* vf = a.vt + kvh * DH * a.Sp;
 
@@ -133,7 +133,7 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   // DMA assignment: instruction i of wave w fills the 64-chunk block b = i * NWAVE + w of a ring
   // step (block sizes are multiples of NWAVE, so the key group and the K / V^T role of instruction i
   // are compile-time). Per ring step only the tile origin k0 changes: a chunk at key j < P comes
-  // from the cache, j < P + S from the fresh keys/values. A chunk past the last key re-reads the
+  // from the cache, j < P + Sk from the fresh keys/values. A chunk past the last key re-reads the
   // last key's (or last 8-key chunk's) data: those keys score -inf, so their probability is
   // exactly 0 against finite values, and the address stays branch-free.
   static_assert((KCH / 64) % NWAVE == 0 && (VCH / 64) % NWAVE == 0, "DMA blocks per wave");
@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(NQ * KG * 64) attn_kernel(AttnArgs a) {
   }
   const uint32_t lds_base = lds_addr_of(sm) + (uint32_t)wid * 1024u;
   const int klast = nkeys - 1, vlast = (nkeys - 1) & ~7;  // last key, start of the last 8-key chunk
-  const int vlast_f = (S - 1) & ~7;                          // the same for the fresh values alone
+  const int vlast_f = (Sk - 1) & ~7;                         // the same for the fresh values alone
   // the main loop below is instantiated twice: without (kFresh) and with a cached prefix
   auto main_loop = [&](auto fresh_only) {
     constexpr bool kFresh = decltype(fresh_only)::value;
@@ -386,31 +386,65 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
 
 // ---------------------------------------------------------------- cache write-back
 // One thread per 16-byte key chunk, then one per value element (the value rows are key-contiguous
-// and the write offset P + s need not be 8-aligned at a ragged S).
+// and the write offset P + s need not be 8-aligned). Token s of the step sits in slot koff + s of the
+// fresh buffers (k rows of Sk keys, v^T rows of pitch Sp).
 __global__ void __launch_bounds__(256) kv_writeback_kernel(const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
                                                           bf16_t* __restrict__ kc, bf16_t* __restrict__ vc, int BH,
-                                                          int S, int Sp, int dh, int P, int Pc) {
+                                                          int S, int Sk, int Sp, int koff, int dh, int P, int Pc) {
   const size_t nk = (size_t)BH * S * (dh / 8), nv = (size_t)BH * dh * S;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nk + nv; i += (size_t)gridDim.x * blockDim.x) {
     if (i < nk) {
       const size_t c = i % (dh / 8), rest = i / (dh / 8);
       const size_t s = rest % S, bh = rest / S;
       *reinterpret_cast<uint4*>(kc + (bh * Pc + P + s) * dh + 8 * c) =
-          *reinterpret_cast<const uint4*>(k + (bh * S + s) * dh + 8 * c);
+          *reinterpret_cast<const uint4*>(k + (bh * Sk + koff + s) * dh + 8 * c);
     } else {
       const size_t e = i - nk;
       const size_t s = e % S, rest = e / S;  // rest = bh * dh + d
-      vc[rest * Pc + P + s] = vt[rest * Sp + s];
+      vc[rest * Pc + P + s] = vt[rest * Sp + koff + s];
     }
   }
 }
 
-void launch_kv_writeback(const bf16_t* k, const bf16_t* vt, bf16_t* kc, bf16_t* vc, int B, int Hkv, int S, int Sp,
-                         int dh, int P, int Pc, hipStream_t s) {
+void launch_kv_writeback(const bf16_t* k, const bf16_t* vt, bf16_t* kc, bf16_t* vc, int B, int Hkv, int S, int Sk,
+                         int Sp, int koff, int dh, int P, int Pc, hipStream_t s) {
   const size_t n = (size_t)B * Hkv * S * (dh / 8 + dh);
   if (n == 0) return;
   const int grid = (int)((n + 255) / 256 < 8 * 1024 ? (n + 255) / 256 : 8 * 1024);
-  hipLaunchKernelGGL(kv_writeback_kernel, dim3(grid), dim3(256), 0, s, k, vt, kc, vc, B * Hkv, S, Sp, dh, P, Pc);
+  hipLaunchKernelGGL(kv_writeback_kernel, dim3(grid), dim3(256), 0, s, k, vt, kc, vc, B * Hkv, S, Sk, Sp, koff, dh, P,
+                     Pc);
+}
+
+// ---------------------------------------------------------------- carried cache keys
+// A cached prefix whose length P is not a multiple of 8 ends inside an 8-key chunk. Attention reads the
+// cache only in whole chunks, so the koff = P mod 8 newest cached keys (and values) are copied in front
+// of the fresh ones: slots [0, koff) of k [BH, Sk, dh] and of every v^T row (pitch Sp). One thread per
+// element.
+__global__ void __launch_bounds__(256) kv_carry_kernel(const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+                                                      bf16_t* __restrict__ k, bf16_t* __restrict__ vt, int BH, int Sk,
+                                                      int Sp, int dh, int P, int Pc, int koff) {
+  const size_t n = (size_t)BH * koff * dh;  // as many key elements as value elements
+  const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (i >= 2 * n) return;
+  const int P8 = P - koff;
+  if (i < n) {
+    const size_t d = i % dh, rest = i / dh;
+    const size_t j = rest % koff, bh = rest / koff;
+    k[(bh * Sk + j) * dh + d] = kc[(bh * Pc + P8 + j) * dh + d];
+  } else {
+    const size_t e = i - n;
+    const size_t j = e % koff, rest = e / koff;  // rest = bh * dh + d
+    vt[rest * Sp + j] = vc[rest * Pc + P8 + j];
+  }
+}
+
+void launch_kv_carry(const bf16_t* kc, const bf16_t* vc, bf16_t* k, bf16_t* vt, int B, int Hkv, int Sk, int Sp,
+                     int dh, int P, int Pc, hipStream_t s) {
+  const int koff = P % 8;
+  if (koff == 0) return;
+  const size_t n = 2 * (size_t)B * Hkv * koff * dh;
+  hipLaunchKernelGGL(kv_carry_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, kc, vc, k, vt, B * Hkv, Sk,
+                     Sp, dh, P, Pc, koff);
 }
 
 

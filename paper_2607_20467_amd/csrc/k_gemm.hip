@@ -90,6 +90,7 @@ struct EpiQkv {
     constexpr int HALF = DH / 2, LOG2DH = DH == 128 ? 7 : 6;
     static_assert(DH == 64 || DH == 128, "head_dim");
     const int qrows = o.H * DH, krows = o.Hkv * DH;
+    const int Sk = o.Sk ? o.Sk : o.S;  // fresh key rows per (sequence, kv head); token s sits in slot koff + s
     const int wq = wb + 4 * (lane >> 4), tl = tb + (lane & 15);
 #pragma unroll
     for (int j = 0; j < ST; ++j) {
@@ -99,8 +100,8 @@ struct EpiQkv {
       const int pos = o.pos0 + s;
       // per token: element offsets of (head 0, position s) in q, k, and of (row 0, key s) in v^T
       const uint32_t qt = (uint32_t)(b * o.H * o.S + s) * DH;
-      const uint32_t kt = (uint32_t)(b * o.Hkv * o.S + s) * DH;
-      const uint32_t vtt = (uint32_t)b * o.Hkv * DH * o.Sp + s;
+      const uint32_t kt = (uint32_t)(b * o.Hkv * Sk + o.koff + s) * DH;
+      const uint32_t vtt = (uint32_t)b * o.Hkv * DH * o.Sp + o.koff + s;
       const float2* rope_t = o.rope ? o.rope + (size_t)pos * HALF : nullptr;
 #pragma unroll
       for (int i = 0; i < SW; ++i) {
@@ -120,7 +121,7 @@ struct EpiQkv {
             const float a1 = v2 * cs1.x - v3 * cs1.y, b1 = v3 * cs1.x + v2 * cs1.y;
             v0 = a0; v1 = b0; v2 = a1; v3 = b1;
           }
-          bf16_t* base = isq ? o.q + qt + (uint32_t)head * o.S * DH : o.k + kt + (uint32_t)head * o.S * DH;
+          bf16_t* base = isq ? o.q + qt + (uint32_t)head * o.S * DH : o.k + kt + (uint32_t)head * Sk * DH;
           *reinterpret_cast<uint32_t*>(base + jp) = f2bf2(v0, v2);
           *reinterpret_cast<uint32_t*>(base + HALF + jp) = f2bf2(v1, v3);
         } else {
@@ -130,8 +131,8 @@ struct EpiQkv {
           base[o.Sp] = f2bf(v1);
           base[2 * o.Sp] = f2bf(v2);
           base[3 * o.Sp] = f2bf(v3);
-          if (s == o.S - 1) {  // the last token also clears the padding keys [S, Sp) of its four rows
-            for (int z = 1; s + z < o.Sp; ++z)
+          if (s == o.S - 1) {  // the last token also clears the padding slots [koff + S, Sp) of its four rows
+            for (int z = 1; o.koff + s + z < o.Sp; ++z)
               for (int rr = 0; rr < 4; ++rr) base[rr * o.Sp + z] = 0;
           }
         }

@@ -320,12 +320,21 @@ void launch_iota(int32_t* rows, int32_t* count, int n, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------- DCV + drafts + remask
+// End of the window for a pointer at `pos`: gen_end, or with semi-AR blocks (block_len > 0, blocks of
+// block_len positions tiling the line from block_origin) the end of the block holding pos, if earlier.
+__device__ __forceinline__ int window_end(int pos, int gen_end, int block_origin, int block_len) {
+  if (block_len <= 0) return gen_end;
+  const long d = (long)pos - block_origin;
+  const long q = d >= 0 ? d / block_len : -((-d + block_len - 1) / block_len);  // floor(d / block_len)
+  return (int)min((long)gen_end, (long)block_origin + (long)block_len * (q + 1));
+}
+
 // One workgroup per sequence.
 __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ tokens, int S, int32_t* __restrict__ p,
-                                                    int gen_end, int L, float tau_c, float tau_d, int mask_id,
-                                                    dcl_row_stats st, int32_t* __restrict__ k_raw,
-                                                    int32_t* __restrict__ k_eff, uint32_t flags,
-                                                    int32_t* __restrict__ k_hist) {
+                                                    int gen_end, int L, int block_origin, int block_len, float tau_c,
+                                                    float tau_d, int mask_id, dcl_row_stats st,
+                                                    int32_t* __restrict__ k_raw, int32_t* __restrict__ k_eff,
+                                                    uint32_t flags, int32_t* __restrict__ k_hist) {
   __shared__ int red[4];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   int32_t* x = tokens + (size_t)b * S;
@@ -343,7 +352,7 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
     }
     return;
   }
-  const int L_eff = min(L, gen_end - pb);
+  const int L_eff = min(L, window_end(pb, gen_end, block_origin, block_len) - pb);
   // window ends computed in 64-bit: p + L may exceed INT_MAX for a huge L
   const int draft_start = (int)min((long)pb + L, (long)gen_end);
   if (flags & DCL_SEL_NONCONTIGUOUS) {
@@ -436,7 +445,7 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
     if ((any || x[j] == mask_id) && conf_at(j) > tau_d && top1[j] >= 0) x[j] = top1[j];
   __syncthreads();
   const int pn = pb + Ke;
-  const int stop = (int)min((long)pn + L, (long)gen_end);
+  const int stop = (int)min((long)pn + L, (long)window_end(pn, gen_end, block_origin, block_len));
   for (int j = pn + tid; j < stop; j += 256) x[j] = mask_id;
   if (tid == 0) {
     p[b] = pn;
@@ -450,22 +459,24 @@ __global__ void __launch_bounds__(256) select_kernel(int32_t* __restrict__ token
 // with 0 <= p_b < gen_end; one workgroup per sequence.
 __global__ void __launch_bounds__(256) remask_kernel(int32_t* __restrict__ tokens, int S,
                                                     const int32_t* __restrict__ p, int gen_end, int L,
-                                                    int mask_id) {
+                                                    int block_origin, int block_len, int mask_id) {
   const int b = blockIdx.x;
   const int pb = p[b];
   if (pb < 0 || pb >= gen_end) return;
-  const int stop = (int)min((long)pb + L, (long)gen_end);
+  const int stop = (int)min((long)pb + L, (long)window_end(pb, gen_end, block_origin, block_len));
   for (int j = pb + (int)threadIdx.x; j < stop; j += 256) tokens[(size_t)b * S + j] = mask_id;
 }
 
-void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, float tau_c, float tau_d,
-                   int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff, uint32_t flags, hipStream_t s,
-                   int32_t* k_hist) {
-  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, tau_c, tau_d, mask_id, st,
-                     k_raw, k_eff, flags, k_hist);
+void launch_select(int32_t* tokens, int B, int S, int32_t* p, int gen_end, int L, int block_origin, int block_len,
+                   float tau_c, float tau_d, int mask_id, dcl_row_stats st, int32_t* k_raw, int32_t* k_eff,
+                   uint32_t flags, hipStream_t s, int32_t* k_hist) {
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, block_origin, block_len,
+                     tau_c, tau_d, mask_id, st, k_raw, k_eff, flags, k_hist);
 }
-void launch_remask(int32_t* tokens, int B, int S, const int32_t* p, int gen_end, int L, int mask_id, hipStream_t s) {
-  hipLaunchKernelGGL(remask_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, mask_id);
+void launch_remask(int32_t* tokens, int B, int S, const int32_t* p, int gen_end, int L, int block_origin,
+                   int block_len, int mask_id, hipStream_t s) {
+  hipLaunchKernelGGL(remask_kernel, dim3(B), dim3(256), 0, s, tokens, S, p, gen_end, L, block_origin, block_len,
+                     mask_id);
 }
 
 // ---------------------------------------------------------------- weight packing (load time)

@@ -86,7 +86,7 @@ def test_step_and_select_argument_checks_without_gpu(dcl):
         r = lib.dcl_denoise_step(m, 8, 1, 384, 8, 384, None, 0, st, 256, 1 << 40, None)
         assert r == 5 and "not loaded" in dcl.dcl_last_error()
         steps = ctypes.c_int32(-1)
-        r = lib.dcl_generate(m, 8, 1, 384, 8, 384, None, 0, 32, 0.7, 0.98, 0, 10, 1, st, None, None, None, 256,
+        r = lib.dcl_generate(m, 8, 1, 384, 8, 384, None, 0, 32, 0, 0, 0.7, 0.98, 0, 10, 1, st, None, None, None, 256,
                              1 << 40, ctypes.byref(steps), None)
         assert r == 5 and "not loaded" in dcl.dcl_last_error()
         # load: misaligned / too small / wrong count
@@ -100,18 +100,21 @@ def test_step_and_select_argument_checks_without_gpu(dcl):
         dcl.dcl_model_destroy(m)
     sel = lib.dcl_select_contiguous
     st = dcl.binding.DclRowStats(1, 1, 1, 1, 1)
-    assert sel(None, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 0, None) == 1
-    assert sel(8, 1, 8, 8, 9, 4, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # gen_end > S
-    assert sel(8, 1, 8, 8, 8, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # L = 0
-    assert sel(8, 1, 8, 8, 8, 4, 1.5, 0.98, 3, st, None, None, 0, None) == 1      # tau_commit > 1
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, -0.1, 3, st, None, None, 0, None) == 1      # tau_draft < 0
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 64, None) == 1     # unknown flag
+    assert sel(None, 1, 8, 8, 8, 4, 0, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1
+    assert sel(8, 1, 8, 8, 9, 4, 0, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # gen_end > S
+    assert sel(8, 1, 8, 8, 8, 0, 0, 0, 0.7, 0.98, 3, st, None, None, 0, None) == 1      # L = 0
+    assert sel(8, 1, 8, 8, 8, 4, 0, 0, 1.5, 0.98, 3, st, None, None, 0, None) == 1      # tau_commit > 1
+    assert sel(8, 1, 8, 8, 8, 4, 0, 0, 0.7, -0.1, 3, st, None, None, 0, None) == 1      # tau_draft < 0
+    assert sel(8, 1, 8, 8, 8, 4, 0, 0, 0.7, 0.98, 3, st, None, None, 64, None) == 1     # unknown flag
     assert "flags" in dcl.dcl_last_error()
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 4 | 2, None) == 1  # non-contiguous + score-all
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, st, None, None, 4 | 8, None) == 1  # non-contiguous + chain drafts
+    assert sel(8, 1, 8, 8, 8, 4, 0, 0, 0.7, 0.98, 3, st, None, None, 4 | 2, None) == 1  # non-contiguous + score-all
+    assert sel(8, 1, 8, 8, 8, 4, 0, 0, 0.7, 0.98, 3, st, None, None, 4 | 8, None) == 1  # non-contiguous + chain drafts
     assert "NONCONTIGUOUS" in dcl.dcl_last_error()
+    assert sel(8, 1, 8, 8, 8, 4, 0, -1, 0.7, 0.98, 3, st, None, None, 0, None) == 1   # block_len < 0
+    assert sel(8, 1, 8, 8, 8, 4, 9, 4, 0.7, 0.98, 3, st, None, None, 0, None) == 1    # block origin > S
+    assert "block" in dcl.dcl_last_error()
     bad = dcl.binding.DclRowStats(0, 1, 0, 1, 1)
-    assert sel(8, 1, 8, 8, 8, 4, 0.7, 0.98, 3, bad, None, None, 0, None) == 1
+    assert sel(8, 1, 8, 8, 8, 4, 0, 0, 0.7, 0.98, 3, bad, None, None, 0, None) == 1
 
 
 def test_product_has_no_oracle_dependency():

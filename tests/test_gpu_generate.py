@@ -33,16 +33,17 @@ def _setup(key, gen_len=48, batch=None):
     return w, run, x, p
 
 
-def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0, kv=None):
+def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0, kv=None, block_origin=0, block_len=0):
     """States after each of n_iter eager iterations (device-resident, synchronised between them)."""
     import torch
     import paper_2607_20467_amd as dcl
+    from oracle.select import block_end
     B, S = x0.shape
     tok, p = to_dev(x0), to_dev(p0)
     # Algorithm 1's loop-top remask of the first window (the initial masks already cover it)
     xs = tok.cpu().numpy()
     for b in range(B):
-        xs[b, p0[b]:min(p0[b] + L, S)] = w.geom.mask_id
+        xs[b, p0[b]:min(p0[b] + L, block_end(int(p0[b]), S, block_origin, block_len))] = w.geom.mask_id
     tok.copy_(to_dev(xs))
     st = run.new_stats(B, S)
     kr = torch.zeros(B, dtype=torch.int32, device="cuda")
@@ -50,14 +51,15 @@ def _eager(run, w, x0, p0, L, tc, td, n_iter, score_flags=0, select_flags=0, kv=
     out = []
     for _ in range(n_iter):
         run.step(tok, p, S, stats=st, flags=score_flags, kv=kv)
-        dcl.dcl_select_contiguous(tok, B, S, p, S, L, tc, td, w.geom.mask_id, st, kr, ke, select_flags)
+        dcl.dcl_select_contiguous(tok, B, S, p, S, L, tc, td, w.geom.mask_id, st, kr, ke, select_flags,
+                                  block_origin=block_origin, block_len=block_len)
         torch.cuda.synchronize()
         out.append((tok.cpu().numpy(), p.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()))
     return out
 
 
 def _generate(run, w, x0, p0, L, tc, td, max_steps, check_every=1, score_flags=0, select_flags=0, hist=None,
-              kv=None):
+              kv=None, block_origin=0, block_len=0):
     import torch
     import paper_2607_20467_amd as dcl
     B, S = x0.shape
@@ -67,7 +69,7 @@ def _generate(run, w, x0, p0, L, tc, td, max_steps, check_every=1, score_flags=0
     ke = torch.zeros(B, dtype=torch.int32, device="cuda")
     ws, n = run.workspace(B, S, 0 if kv is None else kv[2])
     steps = dcl.dcl_generate(run.model, tok, B, S, p, S, kv, score_flags, L, tc, td, select_flags, max_steps,
-                             check_every, st, kr, ke, hist, ws, n)
+                             check_every, st, kr, ke, hist, ws, n, block_origin=block_origin, block_len=block_len)
     torch.cuda.synchronize()
     return steps, tok.cpu().numpy(), p.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()
 
@@ -178,3 +180,73 @@ def test_cached_prefix_replays_match_the_eager_loop():
     _generate(run, w, x, p, L, tc, td, max_steps=1000, kv=kv)
     torch.cuda.synchronize()
     assert all(torch.equal(a, b) for a, b in zip(ks, ks2))
+
+
+def test_blocked_generation_replays_the_eager_loop():
+    """dcl_generate with semi-autoregressive blocks (block origin at the prompt end, blocks of 8, window 16)
+    reproduces the eager blocked loop bit for bit and finishes at the same iteration."""
+    w, run, x0, p0 = _setup("c1s")
+    L, tc, td, BL = 16, 0.6, 0.9, 8
+    N, S = int(p0[0]), x0.shape[1]
+    ref = _eager(run, w, x0, p0, L, tc, td, 48, block_origin=N, block_len=BL)
+    n_done = next(i + 1 for i, (_, p, _, _) in enumerate(ref) if (p >= S).all())
+    for k in (1, 2, n_done // 2, n_done):
+        steps, tok, p, kr, ke = _generate(run, w, x0, p0, L, tc, td, max_steps=k, block_origin=N, block_len=BL)
+        assert steps == k
+        for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), (tok, p, kr, ke), ref[k - 1]):
+            np.testing.assert_array_equal(g, r, err_msg=f"{name} after {k} blocked iterations")
+    # every block end is reached: p never jumps over one
+    for b in range(x0.shape[0]):
+        visited = {int(r[1][b]) for r in ref[:n_done]}
+        assert {N + BL * j for j in range(1, (S - N) // BL + 1)} <= visited
+
+
+@pytest.mark.parametrize("key,block_len", [("c1", 0), ("c1", 16), ("c1s", 0), ("c1s", 16)])
+def test_whole_trajectory_against_oracle_generate(tiny_weights, key, block_len):
+    """Algorithm 1 end to end on the GPU against oracle.generate from the same prompt (64 generated tokens,
+    window 16, tau_c 0.7, tau_d 0.98; blocks of 16 or none), compared iteration by iteration. Either the
+    trajectories are equal, or the first iteration where they part is reported with what decided it: an
+    acceptance length set by a window row whose oracle confidence lies within that state's derived
+    confidence tolerance of tau_c, a committed id at a near-tie row, or a draft decision at a row within the
+    tolerance of tau_d. The GPU and the oracle start that iteration from the same state."""
+    import oracle
+    from helpers import derived_tolerance
+    w, stored, Wv = tiny_weights(key)
+    M, L, tc, td = 64, 16, 0.7, 0.98
+    _, run, x0, p0 = _setup(key, gen_len=M)
+    N = int(p0[0])
+    S = x0.shape[1]
+    prompt = x0[:, :N]
+    trace = []
+    x_or, steps_or = oracle.generate(w.geom, Wv, prompt, M, L, tc, td, trace=trace, block_len=block_len)
+    gpu = _eager(run, w, x0, p0, L, tc, td, len(trace) + 8, block_origin=N, block_len=block_len)
+    steps_gpu = next(i + 1 for i, (_, p, _, _) in enumerate(gpu) if (p >= S).all())
+    prev_x = x0.copy()
+    prev_p = p0.astype(np.int64)
+    for it, ((gx, gp, gkr, gke), (ox, op, okr, oke)) in enumerate(zip(gpu, trace)):
+        if np.array_equal(gx, ox) and np.array_equal(gp, op):
+            prev_x, prev_p = ox, op
+            continue
+        ref = oracle.step(w.geom, Wv, prev_x, prev_p, S)
+        ct, lt = derived_tolerance(w.geom, Wv, prev_x, prev_p, S, ref)
+        gap = np.log(np.maximum(ref["conf"], 1e-300)) - np.log(np.maximum(ref["p2"], 1e-300))
+        for b in range(x0.shape[0]):
+            if gkr[b] != okr[b]:
+                j = int(prev_p[b]) + min(int(gkr[b]), int(okr[b]))
+                d = abs(ref["conf"][b, j] - tc)
+                print(f"{key} blocks {block_len}: iteration {it + 1} of {steps_or}, seq {b}: K GPU {gkr[b]}, oracle "
+                      f"{okr[b]}; deciding row {j}: oracle conf {ref['conf'][b, j]:.5f}, |c - tau_c| = {d:.5f} "
+                      f"(state's confidence tolerance {ct:.5f})", flush=True)
+                assert d <= ct
+                continue
+            for j in np.nonzero(gx[b] != ox[b])[0]:
+                committed = prev_p[b] <= j < op[b]
+                why = (f"top-1/top-2 logit gap {gap[b, j]:.4f} (tolerance {lt:.4f})" if committed else
+                       f"draft row: |c - tau_d| = {abs(ref['conf'][b, j] - td):.5f}, gap {gap[b, j]:.4f}")
+                print(f"{key} blocks {block_len}: iteration {it + 1} of {steps_or}, seq {b}: token at {j} differs, "
+                      f"{why}", flush=True)
+                assert gap[b, j] < lt or (not committed and abs(ref["conf"][b, j] - td) <= ct)
+        break
+    else:
+        assert steps_gpu == steps_or and np.array_equal(gpu[steps_gpu - 1][0], x_or)
+        print(f"{key} blocks {block_len}: the GPU trajectory equals the oracle's ({steps_or} iterations)", flush=True)

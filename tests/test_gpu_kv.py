@@ -107,3 +107,105 @@ def test_layer0_keys_values_match_oracle(key):
                   % ((diff == 0).mean(), (diff / bound).max()), flush=True)
             assert (diff == 0).mean() > 0.98
             assert (diff <= bound * 1.01).all()
+
+
+class _LayerCase:
+    """The state test_gpu_layers._layer_step needs, for a cached step of a small model (every row checked)."""
+
+    def __init__(self, w, run, tok, P, kv, kv_host, stored):
+        import torch
+        from oracle.numerics import rope_tables
+        g = w.geom
+        self.w, self.run, self.key = w, run, w.key
+        self.B, self.S = tok.shape
+        self.T, self.P = self.B * self.S, P
+        self.Sp = (P % 8 + self.S + 7) // 8 * 8
+        self.kv, self.kv_host = kv, kv_host
+        from oracle.numerics import weight_values
+        emb = weight_values(stored["embed"][tok]).astype(np.float32)     # the bf16 table the library packs
+        self.r = torch.from_numpy(np.ascontiguousarray(emb.reshape(self.T, g.d_model))).cuda()
+        d, F, hd, kd = g.d_model, g.d_ffn, g.n_heads * g.head_dim, g.n_kv_heads * g.head_dim
+        i16, f32 = torch.int16, torch.float32
+        mk = lambda n, dt: torch.empty(n, dtype=dt, device="cuda")
+        self.taps = {"u": mk(self.T * d, i16), "q": mk(self.T * hd, i16), "k": mk(self.B * (P % 8 + self.S) * kd, i16),
+                     "v": mk(self.B * kd * self.Sp, i16), "o": mk(self.T * hd, i16), "r_mid": mk(self.T * d, f32),
+                     "u2": mk(self.T * d, i16), "a": mk(self.T * F, i16), "r_out": mk(self.T * d, f32)}
+        self.cos, self.sin = rope_tables(P + np.arange(self.S), g.head_dim, g.rope_base)
+        self.reports = []
+
+    def sample_rows(self, l):
+        return np.arange(self.T)
+
+
+@pytest.mark.parametrize("key", list(CASES))
+def test_committed_span_append_then_ragged_cached_step(key):
+    """f3 end to end with prefix lengths that are not multiples of 8: cache the first 37 positions (refresh),
+    run a cached step over the rest, commit its K_eff tokens, append them to the cache (prefix 37 + K), and
+    run the next cached step over the remaining tokens.
+    * The appended keys/values equal, bit for bit, the ones the forward of those tokens over the 37-position
+      cache computes (dcl_debug_layer, every layer).
+    * The cached step after the append is checked stage by stage at every layer (stage_checks.py; attention
+      over [GPU cache || fresh keys]), and its statistics against the oracle's step over the same cache
+      within the whole-step tolerance."""
+    import torch
+    import paper_2607_20467_amd as dcl
+    from test_gpu_layers import _layer_step, _layer_weights
+    w, stored, W, run = _setup(key)
+    g = w.geom
+    tok, _ = synth.initial_state(w)
+    B, S_all = tok.shape
+    P0, cap = 37, 104
+    ks, vs = _new_cache(g, B, cap, fill=0x7FC0)               # unused slots hold NaN bit patterns
+    run.kv_append(to_dev(tok[:, :P0]), (ks, vs, 0, cap))      # refresh: the prefix's keys/values
+    fresh = tok[:, P0:].copy()
+    fresh[:, :16] = g.mask_id                                 # the window at the first fresh position is masked
+    Sf = fresh.shape[1]
+    t_dev, p_dev = to_dev(fresh), to_dev(np.zeros(B, np.int32))
+    st = run.step(t_dev, p_dev, Sf, kv=(ks, vs, P0, cap))
+    kr = torch.zeros(B, dtype=torch.int32, device="cuda")
+    ke = torch.zeros(B, dtype=torch.int32, device="cuda")
+    dcl.dcl_select_contiguous(t_dev, B, Sf, p_dev, Sf, 16, 0.5, 0.98, g.mask_id, st, kr, ke)
+    torch.cuda.synchronize()
+    K = int(ke.cpu().numpy().min())
+    committed = t_dev.cpu().numpy()
+    print(f"case {key}: prefix {P0}, K_eff {ke.cpu().tolist()}, appending {K} committed tokens", flush=True)
+    assert K >= 1
+    # (a) the append writes what the forward of those tokens over the cache computes
+    k_before = [k.clone() for k in ks]
+    v_before = [v.clone() for v in vs]
+    run.kv_append(to_dev(committed[:, :K]), (ks, vs, P0, cap))
+    P1 = P0 + K
+    ref_case = _LayerCase(w, run, committed[:, :K], P0, (k_before, v_before, P0, cap), None, stored)
+    ws, n = run.workspace(B, K, P0)
+    koff = P0 % 8
+    for l in range(g.n_layers):
+        dcl.dcl_debug_layer(run.model, B, K, (k_before, v_before, P0, cap), l, ref_case.r, ref_case.taps, ws, n)
+        kt = ref_case.taps["k"].view(B, g.n_kv_heads, koff + K, g.head_dim)[:, :, koff:]
+        vt = ref_case.taps["v"].view(B, g.n_kv_heads, g.head_dim, ref_case.Sp)[:, :, :, koff:koff + K]
+        assert torch.equal(ks[l][:, :, P0:P1], kt), f"layer {l}: appended keys differ"
+        assert torch.equal(vs[l][:, :, :, P0:P1], vt), f"layer {l}: appended values differ"
+        assert torch.equal(ks[l][:, :, :P0], k_before[l][:, :, :P0])
+        assert torch.equal(ks[l][:, :, P1:], k_before[l][:, :, P1:])
+        ref_case.r.copy_(ref_case.taps["r_out"].view(ref_case.T, g.d_model))
+    # (b) the next cached step, prefix P1 (not a multiple of 8), stage by stage
+    rest = committed[:, K:].copy()
+    kv_host = [(ks[l].cpu().numpy().view(np.uint16), vs[l].cpu().numpy().view(np.uint16)) for l in range(g.n_layers)]
+    case = _LayerCase(w, run, rest, P1, (ks, vs, P1, cap), kv_host, stored)
+    for l in range(g.n_layers):
+        rep = _layer_step(case, l, _layer_weights(W, g, l))
+        print(f"{key} prefix {P1} layer {l}: ok, flips " +
+              ", ".join(f"{k} {v['flip_fraction']:.4f}" for k, v in rep.items() if isinstance(v, dict) and "flips" in v),
+              flush=True)
+    # (c) whole step over the same cache against the oracle
+    Sr = rest.shape[1]
+    t2, p2 = to_dev(rest), to_dev(np.zeros(B, np.int32))
+    gpu = stats_to_np(run.step(t2, p2, Sr, kv=(ks, vs, P1, cap)))
+
+    def kvf(b, l):
+        kk, vv = kv_host[l]
+        return synth.bf16_bits_to_f32(kk[b][:, :P1]), synth.bf16_bits_to_f32(vv[b][:, :, :P1])
+    kvf.prefix = P1
+    ref = oracle.step(g, W, rest, np.zeros(B, np.int64), Sr, kv=kvf)
+    ct, lt = derived_tolerance(g, W, rest, np.zeros(B, np.int64), Sr, ref, kv=kvf)
+    compare_stats(gpu, ref, 0.5, 0.98, what=f"{key} cached step after the append (prefix {P1})", conf_tol=ct,
+                  logit_tol=lt)

@@ -58,8 +58,8 @@ class _Case:
         w, g = self.w, self.w.geom
         self.tok, self.p = synth.initial_state(w)
         self.B, self.S = self.tok.shape
-        self.T, self.Sp = self.B * self.S, (self.S + 7) // 8 * 8
         self.P = w.kv_prefix
+        self.T, self.Sp = self.B * self.S, (self.P % 8 + self.S + 7) // 8 * 8
         self.kv_host = None
         self.kv = None
         if self.P:
@@ -73,7 +73,7 @@ class _Case:
         i16, f32 = torch.int16, torch.float32
         self.taps = {"u": torch.empty(self.T * d, dtype=i16, device="cuda"),
                      "q": torch.empty(self.T * hd, dtype=i16, device="cuda"),
-                     "k": torch.empty(self.T * kd, dtype=i16, device="cuda"),
+                     "k": torch.empty(self.B * (self.P % 8 + self.S) * kd, dtype=i16, device="cuda"),
                      "v": torch.empty(self.B * kd * self.Sp, dtype=i16, device="cuda"),
                      "o": torch.empty(self.T * hd, dtype=i16, device="cuda"),
                      "r_mid": torch.empty(self.T * d, dtype=f32, device="cuda"),
@@ -112,8 +112,9 @@ def _layer_step(case, l, Wl):
     r_out = host("r_out", d).astype(np.float64)
     o = host("o", H * dh)
     q_all = case.taps["q"].view(case.B, H, case.S, dh)
-    k_all = case.taps["k"].view(case.B, Hkv, case.S, dh).cpu().numpy()
-    v_all = case.taps["v"].view(case.B, Hkv, dh, case.Sp).cpu().numpy()
+    koff = case.P % 8                    # slots of the newest cached keys carried in front of the fresh ones
+    k_all = case.taps["k"].view(case.B, Hkv, koff + case.S, dh)[:, :, koff:].cpu().numpy()
+    v_all = case.taps["v"].view(case.B, Hkv, dh, case.Sp)[:, :, :, koff:koff + case.S].cpu().numpy()
     q = q_all[torch.from_numpy(bs).cuda(), :, torch.from_numpy(ss).cuda()].cpu().numpy()   # [n, H, dh]
     W = lambda name: Wl[name]
     p_ = f"l{l}."
@@ -148,11 +149,11 @@ def _layer_step(case, l, Wl):
     for b in np.unique(bs):
         sel = np.nonzero(bs == b)[0]
         kb = sc.bf16_bits_to_f64(k_all[b])                               # [Hkv, S, dh]
-        vb = sc.bf16_bits_to_f64(v_all[b][:, :, :case.S]).transpose(0, 2, 1)
+        vb = sc.bf16_bits_to_f64(v_all[b]).transpose(0, 2, 1)
         if case.P:
-            kc, vc = case.kv_host[l]
-            kb = np.concatenate([sc.bf16_bits_to_f64(kc[b]), kb], axis=1)
-            vb = np.concatenate([sc.bf16_bits_to_f64(vc[b]).transpose(0, 2, 1), vb], axis=1)
+            kc, vc = case.kv_host[l]                                     # cache buffers; positions [0, P) in use
+            kb = np.concatenate([sc.bf16_bits_to_f64(kc[b][:, :case.P]), kb], axis=1)
+            vb = np.concatenate([sc.bf16_bits_to_f64(vc[b][:, :, :case.P]).transpose(0, 2, 1), vb], axis=1)
         qb = qf[sel].transpose(1, 0, 2)                                  # [H, m, dh]
         ex_o[sel] = attention_stage(g, qb, kb, vb, _ident)
         for h in range(H):

@@ -8,7 +8,7 @@ from oracle.select import scored_mask
 pytestmark = pytest.mark.gpu
 
 
-def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0, p2=None):
+def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0, p2=None, block_origin=0, block_len=0):
     import torch
     import paper_2607_20467_amd as dcl
     B, S = tok.shape
@@ -21,7 +21,8 @@ def _run_gpu(tok, p, end, L, tc, td, mask, top1, conf, flags=0, p2=None):
           "lse": torch.zeros((B, S), dtype=torch.float32, device="cuda")}
     kr = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     ke = torch.full((B,), -7, dtype=torch.int32, device="cuda")
-    dcl.dcl_select_contiguous(t, B, S, pp, end, L, tc, td, mask, st, kr, ke, flags)
+    dcl.dcl_select_contiguous(t, B, S, pp, end, L, tc, td, mask, st, kr, ke, flags, block_origin=block_origin,
+                              block_len=block_len)
     torch.cuda.synchronize()
     return t.cpu().numpy(), pp.cpu().numpy(), kr.cpu().numpy(), ke.cpu().numpy()
 
@@ -59,7 +60,8 @@ def test_select_golden_cases():
     cases = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "select_cases.json")))["select_cases"]
     for c in cases:
         got = _run_gpu(np.array([c["tokens"]]), np.array([c["p"]]), c["gen_end"], c["L"], c["tau_commit"],
-                       c["tau_draft"], c["mask_id"], np.array([c["top1"]]), np.array([c["conf"]], np.float32))
+                       c["tau_draft"], c["mask_id"], np.array([c["top1"]]), np.array([c["conf"]], np.float32),
+                       block_origin=c.get("block_origin", 0), block_len=c.get("block_len", 0))
         assert got[0][0].tolist() == c["expect_tokens"], c["name"]
         assert (got[1][0], got[2][0], got[3][0]) == (c["expect_p"], c["expect_K_raw"], c["expect_K_eff"]), c["name"]
 
@@ -180,3 +182,34 @@ def test_select_degenerate_thresholds_and_windows(tc, L):
         np.testing.assert_array_equal(got[2][live], 0)
         np.testing.assert_array_equal(got[3][live], 1)
     np.testing.assert_array_equal(got[1][~live], p[~live])      # a finished sequence does not move
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_select_with_semi_ar_blocks_bit_exact(seed):
+    """Semi-autoregressive blocks (reading R24): the window and its re-mask stop at the end of p's block,
+    with blocks shorter and longer than the window, origins before and inside the state, every flag."""
+    rng = np.random.default_rng(300 + seed)
+    mask = 4095
+    B, S = int(rng.integers(1, 9)), int(rng.integers(16, 600))
+    end = int(rng.integers(8, S + 1))
+    L = int(rng.choice([1, 8, 16, 32, 128]))
+    BL = int(rng.choice([1, 5, 16, 32, 64]))
+    origin = int(rng.integers(0, end))
+    tok = rng.integers(0, 4000, (B, S))
+    p = rng.integers(max(origin - 3, 0), end + 1, B)
+    for b in range(B):
+        tok[b, p[b]:] = np.where(rng.random(S - p[b]) < 0.6, mask, tok[b, p[b]:])
+        tok[b, p[b]:min(p[b] + L, end)] = mask
+    for flags, score_all in ((0, False), (1, False), (2, True)):
+        sc = scored_mask(tok, p, end, mask, score_all)
+        conf = np.where(sc, rng.uniform(0, 1, (B, S)).astype(np.float32), np.float32(-1)).astype(np.float32)
+        conf[sc & (rng.random((B, S)) < 0.05)] = np.float32(0.7)
+        top1 = np.where(sc, rng.integers(0, 4000, (B, S)), -1)
+        tc, td = np.float32(0.7), np.float32(rng.choice([0.5, 0.9, 1.5]))
+        ref = oracle.select_contiguous(tok, p, end, L, float(tc), float(td), mask, top1, conf.astype(np.float64),
+                                       no_progress_guard=bool(flags & 1), score_all=score_all,
+                                       block_origin=origin, block_len=BL)
+        got = _run_gpu(tok, p, end, L, float(tc), float(td), mask, top1, conf, flags, block_origin=origin,
+                       block_len=BL)
+        for name, g, r in zip(("tokens", "p", "K_raw", "K_eff"), got, ref):
+            np.testing.assert_array_equal(g, r, err_msg=f"{name} flags={flags} B={B} S={S} L={L} blocks {origin}+{BL}")
