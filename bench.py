@@ -235,6 +235,9 @@ def main():
                          "threshold rule, or drafts restricted to the leading chain")
     ap.add_argument("--score-all", action="store_true", help="score every uncommitted position, not only masks")
     ap.add_argument("--suppress-mask", action="store_true", help="leave the [MASK] id out of the vocabulary")
+    ap.add_argument("--graph", choices=("auto", "on", "off"), default="auto",
+                    help="also time the step replayed from a captured HIP graph and report that rate (auto: for the "
+                         "launch-bound tiny workload c1)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB (hardware-counter calibration)")
     ap.add_argument("--pmc-summary", metavar="CSV", help="summarise a rocprofv3 --pmc counter_collection.csv "
@@ -289,12 +292,13 @@ def main():
     k_eff = torch.zeros(B, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
 
-    def one_step():
+    def one_step(st=None):
+        st = stream if st is None else st
         tok.copy_(tok0, non_blocking=True)
         p.copy_(p0, non_blocking=True)
-        dcl.dcl_denoise_step(run.model, tok, B, S, p, w.gen_end, kv, score_flags, stats, ws, ws_bytes, stream)
+        dcl.dcl_denoise_step(run.model, tok, B, S, p, w.gen_end, kv, score_flags, stats, ws, ws_bytes, st)
         dcl.dcl_select_contiguous(tok, B, S, p, w.gen_end, w.window, w.tau_commit, w.tau_draft, g.mask_id, stats,
-                                  k_raw, k_eff, sel_flags, stream)
+                                  k_raw, k_eff, sel_flags, st)
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
@@ -313,6 +317,31 @@ def main():
     step_ms = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     clock = gpu_clock_mhz()
     ms = 1000.0 * elapsed / args.steps
+    launch = {"mode": "eager", "eager_ms_per_step": round(ms, 4)}
+    if args.graph == "on" or (args.graph == "auto" and w.key == "c1"):
+        # the same step captured once into a HIP graph (torch's CUDAGraph on a side stream) and replayed:
+        # for a launch-latency-bound step this removes the per-kernel host launch cost
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(graph, stream=side):
+                one_step(side)
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        evs[0].record(stream)
+        for i in range(args.steps):
+            graph.replay()
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        step_ms = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+        ms = 1000.0 * elapsed / args.steps
+        launch.update(mode="hip graph replay", graph_ms_per_step=round(ms, 4))
+        log(f"eager {launch['eager_ms_per_step']:.4f} ms/step, graph replay {ms:.4f} ms/step")
     steps_per_s = 1000.0 / ms
     flops = step_flops(w, R)
     mfma_util = 100.0 * flops / (ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12)
@@ -341,6 +370,8 @@ def main():
             classes[name] = ent
             log(f"  {name:22s} {n / args.steps:6.1f} launches/step  avg {avg_us:9.2f} us  "
                 f"{tms / args.steps:8.3f} ms/step" + (f"  {ent['tflops']:7.1f} TFLOP/s" if "tflops" in ent else ""))
+        launch["kernels_per_step"] = round(sum(e["launches_per_step"] for e in classes.values()), 2)
+        launch["event_timed_kernel_ms_per_step"] = round(sum(e["ms_per_step"] for e in classes.values()), 4)
         alg_bytes = step_bytes(w, R)
         for name, ent in classes.items():
             if name in alg_bytes:
@@ -408,6 +439,7 @@ def main():
         "step_ms": {"median": round(float(np.median(step_ms)), 4), "p10": round(float(np.percentile(step_ms, 10)), 4),
                     "p90": round(float(np.percentile(step_ms, 90)), 4)},
         "gpu_sclk_mhz": clock,
+        "launch": launch,
         "scored_tokens_per_s": round(R * steps_per_s, 1),
         "mfma_util_pct": round(mfma_util, 2),
         "tflop_per_step": round(flops / 1e12, 4),

@@ -255,10 +255,30 @@ def random_drafts(w: Workload) -> np.ndarray:
     return out
 
 
+_STORED = os.path.join(os.path.dirname(_HERE), "tests", "golden")
+
+
+def stored_drafts(w: Workload) -> Optional[np.ndarray]:
+    """[B, n_draft] draft ids stored for this workload (``{key}_drafts.json``, written from earlier
+    predictions by the golden-value script), or None when there are none for its geometry and region."""
+    import json
+    path = os.path.join(_STORED, f"{w.key}_drafts.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    d = np.asarray(rec["drafts"], np.int32)
+    if rec.get("geometry") != w.geom.name or list(rec.get("draft_region", [])) != list(w.draft) or \
+            d.shape != (w.batch, w.draft[1] - w.draft[0]):
+        return None
+    return d
+
+
 def initial_state(w: Workload, drafts: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
     """(tokens [B,S] int32, p [B] int32): prompt, then mask ids; draft region filled if given.
 
-    With ``drafts=None`` and a non-empty draft region the seeded random stand-ins are used.
+    With ``drafts=None`` and a non-empty draft region, the stored drafts of the workload (earlier
+    predictions, ``stored_drafts``) are used when there are some, the seeded random stand-ins otherwise.
     """
     B, S, mask = w.batch, w.seq, w.geom.mask_id
     tok = np.full((B, S), mask, np.int32)
@@ -266,6 +286,8 @@ def initial_state(w: Workload, drafts: Optional[np.ndarray] = None) -> Tuple[np.
         tok[:, : w.prompt_len] = prompts(w)
     lo, hi = w.draft
     if hi > lo:
+        if drafts is None:
+            drafts = stored_drafts(w)
         tok[:, lo:hi] = random_drafts(w) if drafts is None else drafts
     p = np.full((B,), w.p, np.int32)
     return tok, p

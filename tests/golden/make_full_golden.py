@@ -5,7 +5,8 @@ top1 / top2 / conf / p2 / lse, the drift of the same definition evaluated in flo
 the whole-step tolerance), the oracle's selection on its own statistics, and checksums of a few
 weight tensors so a machine that regenerates different weights is detected.
 
-    python tests/golden/make_full_golden.py [--out DIR] [c2 c3 c4 c5]
+    python tests/golden/make_full_golden.py [--out DIR] [c1 c2 c3 c4 c5]
+(c1: the draft placeholders of the tiny workload, c1_drafts.json)
 (tens of minutes on 8 cores; DIR defaults to this directory)
 """
 import hashlib
@@ -88,9 +89,35 @@ def run(key, stored):
           f"K of the float32 evaluation {kr32.tolist()}", flush=True)
 
 
+def make_drafts(key):
+    """Draft placeholders of a workload whose drafts are the previous step's top-1 predictions: the top-1 of
+    a warm-up step on the same prompt with the whole generation region masked (p at the window start),
+    over the draft region. Written to {key}_drafts.json."""
+    import json
+    w = synth.WORKLOADS[key]
+    g = w.geom
+    prompt = synth.prompts(w)
+    B = prompt.shape[0]
+    x = np.full((B, w.seq), g.mask_id, np.int64)
+    x[:, :w.prompt_len] = prompt
+    p = np.full(B, w.p, np.int64)
+    st = oracle.step(g, WeightView(synth.make_weights(g)), x, p, w.gen_end)
+    lo, hi = w.draft
+    rec = {"_source": "top-1 of a float64 oracle step on the prompt followed by mask ids (tests/golden/"
+                      "make_full_golden.py): the previous step's predictions that the workload places in its "
+                      "draft region", "workload": key, "geometry": g.name, "draft_region": [lo, hi],
+           "drafts": st["top1"][:, lo:hi].tolist(), "confidences": st["conf"][:, lo:hi].round(6).tolist()}
+    with open(os.path.join(OUT, f"{key}_drafts.json"), "w") as f:
+        json.dump(rec, f, indent=1)
+    print(f"{key}: drafts {rec['drafts']}", flush=True)
+
+
 def main(keys):
     cache = {}
     for key in keys:
+        if key == "c1":
+            make_drafts(key)
+            continue
         g = synth.WORKLOADS[key].geom
         if g.name not in cache:
             cache.clear()
