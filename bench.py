@@ -388,26 +388,34 @@ def main():
     gen = None
     if not args.no_generate:
         # Algorithm 1 end to end from the workload's initial state (dcl_generate: graph-replayed
-        # iterations, completion checked on the host after each one)
-        torch.cuda.synchronize()
-        tok.copy_(tok0)
-        p.copy_(p0)
-        hist = torch.zeros(w.window + 1, dtype=torch.int32, device="cuda")
-        max_steps = int(w.gen_end - p_h.min())
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        n_it = dcl.dcl_generate(run.model, tok, B, S, p, w.gen_end, kv, score_flags, w.window, w.tau_commit,
-                                w.tau_draft, sel_flags,
-                                max_steps, 1, stats, k_raw, k_eff, hist, ws, ws_bytes, stream)
-        torch.cuda.synchronize()
-        t_gen = time.perf_counter() - t1
-        new_tok = int((w.gen_end - p_h).clip(min=0).sum())
-        done = bool((p.cpu().numpy() >= w.gen_end).all())
-        gen = {"iterations": n_it, "finished": done, "tokens": new_tok, "seconds": round(t_gen, 4),
-               "tokens_per_s": round(new_tok / t_gen, 1), "tokens_per_iteration": round(new_tok / max(n_it, 1), 3),
-               "ms_per_iteration": round(1000 * t_gen / max(n_it, 1), 4), "k_eff_hist": hist.cpu().tolist()}
-        log(f"generation: {n_it} iterations for {new_tok} tokens in {t_gen:.3f} s "
-            f"({new_tok / t_gen:.0f} tok/s, {1000 * t_gen / max(n_it, 1):.2f} ms/iteration)")
+        # iterations, completion checked on the host after each one): block-free with the workload's
+        # window, then semi-autoregressive blocks of 32 with windows of 32 and 128 (the paper's setup)
+        def generate(L, block_len):
+            torch.cuda.synchronize()
+            tok.copy_(tok0)
+            p.copy_(p0)
+            hist = torch.zeros(L + 1, dtype=torch.int32, device="cuda")
+            max_steps = int(w.gen_end - p_h.min())
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            n_it = dcl.dcl_generate(run.model, tok, B, S, p, w.gen_end, kv, score_flags, L, w.tau_commit,
+                                    w.tau_draft, sel_flags, max_steps, 1, stats, k_raw, k_eff, hist, ws, ws_bytes,
+                                    stream, block_origin=w.prompt_len if not w.kv_prefix else 0,
+                                    block_len=block_len)
+            torch.cuda.synchronize()
+            t_gen = time.perf_counter() - t1
+            new_tok = int((w.gen_end - p_h).clip(min=0).sum())
+            done = bool((p.cpu().numpy() >= w.gen_end).all())
+            rec = {"window": L, "block_len": block_len, "iterations": n_it, "finished": done, "tokens": new_tok,
+                   "seconds": round(t_gen, 4), "tokens_per_s": round(new_tok / t_gen, 1),
+                   "tokens_per_iteration": round(new_tok / max(n_it, 1), 3),
+                   "ms_per_iteration": round(1000 * t_gen / max(n_it, 1), 4), "k_eff_hist": hist.cpu().tolist()}
+            log(f"generation (window {L}, blocks {block_len or 'none'}): {n_it} iterations for {new_tok} tokens "
+                f"in {t_gen:.3f} s ({new_tok / t_gen:.0f} tok/s, {1000 * t_gen / max(n_it, 1):.2f} ms/iteration)")
+            return rec
+
+        gen = generate(w.window, 0)
+        gen["blocked"] = [generate(L, 32) for L in (32, 128)]
 
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * 1024 * 1024 // 4

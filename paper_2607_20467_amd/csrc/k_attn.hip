@@ -372,16 +372,17 @@ static void run_attn(const AttnArgs& a, hipStream_t s) {
   }
 }
 
-// A two-stage ring of 64-key tiles. Few query waves (B * H * S / 16 below 4096): 4 query waves
-// x 2 key groups per workgroup, so each wave walks half the keys and twice as many waves share a
-// CU; many query waves: 8 query waves x 1 group, whose 64 KB ring lets two workgroups share a CU.
-// Measured on MI355X (LLaDA-8B / Dream-7B heads, three-part P): 384 tokens 12.3 us (17.6 with one
-// group of 8), 1280 tokens 89 us (99 with one group of 8), 8 x 64 tokens over a 1216-key cache
-// 36 us (54 with one group of 8), Dream-7B 4 x 768 tokens 100 us (117 with two groups of 4).
+// A two-stage ring of 32-key tiles: 64 KB of LDS for head_dim 128, so two workgroups share a CU. Few query
+// waves (B * H * S / 16 below 4096): 4 query waves x 2 key groups per workgroup, so each wave walks half
+// the keys and twice as many waves share a CU; many query waves: 8 query waves x 1 group. Measured on
+// MI355X (LLaDA-8B / Dream-7B heads, three-part P), per launch, against the same layouts with 64-key
+// tiles (128 KB rings, one workgroup per CU): 384 tokens 12.2 us (12.1), 1280 tokens 73.0 us (87.0),
+// 8 x 64 tokens over a 1216-key cache 34.1 us (35.1), Dream-7B 4 x 768 tokens 88.4 us (95.8).
+// head_dim 64 falls back to 64-key tiles (a 32-key tile has too few 64-chunk blocks for 8 waves).
 void launch_attention(const AttnArgs& a, hipStream_t s) {
   const long query_waves = (long)a.B * a.H * ((a.S + 15) / 16);
-  if (query_waves >= 4096) run_attn<8, 1, 64, 2>(a, s);
-  else run_attn<4, 2, 64, 2>(a, s);
+  if (query_waves >= 4096) run_attn<8, 1, 32, 2>(a, s);
+  else run_attn<4, 2, 32, 2>(a, s);
 }
 
 // ---------------------------------------------------------------- cache write-back
