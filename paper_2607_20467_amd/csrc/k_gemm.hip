@@ -326,7 +326,7 @@ struct EpiLm {
 // buffered per 32-wide K substep: the LDS reads of substep s + 1 are in flight while the MFMAs of
 // substep s run, and the first substep of stage k + 1 is read across the stage boundary.
 //
-// The DMA instructions are issued through dma16 (inline assembly), so the compiler's wait-count
+// The DMA instructions are issued through dma16_lds (inline assembly), so the compiler's wait-count
 // pass does not treat them as pending LDS traffic and keeps its LDS waits fine-grained; their
 // completion is tracked here with vmcnt waits on this wave's own
 // outstanding stages, and a bare s_barrier (no vmcnt(0) fence) publishes a stage to the other
@@ -338,6 +338,11 @@ struct EpiLm {
 // adds the slices in split order, so results are bitwise reproducible. nsplit > 1 is only used with
 // a slice epilogue.
 __device__ __attribute__((aligned(64))) uint4 g_zero_chunk[4];
+
+// dma16_at with the LDS destination already wave-uniform (a scalar register)
+__device__ __forceinline__ void dma16_lds(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr), "v"(g) : "memory", "m0");
+}
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -382,10 +387,12 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
     const int kb = min(nk_all, split * kper);
     const int nk = min(nk_all, kb + kper) - kb;
 
-    // Per-lane element offset of this wave's load instructions (loop invariant; -1 = row outside
-    // the operand) and K offset of its chunk. Instruction i of wave `wid` fills chunks
-    // [(wid*IPW + i)*64, +64) of the stage: all weight chunks or all activation chunks.
-    int off[IPW], kc[IPW];
+    // Per-lane source of this wave's load instructions at K offset 0. A row outside the operand
+    // is clamped to the last valid row: its data only reaches accumulators of rows / tokens that
+    // every epilogue skips, so no zero fill is needed. Without a K tail the source of stage kt is
+    // this pointer plus (kb + kt) * KD elements; with one, chunks past K read the zero chunk.
+    const bf16_t* gsrc[IPW];
+    int kc[IPW];
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const int q = wid * IPW + i;
@@ -393,21 +400,20 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
       const bool isw = q * 64 < BW * CPR;
       const int p2 = isw ? pos : pos - BW * CPR;
       const int row = p2 / CPR, c = (p2 % CPR) ^ (row & (CPR - 1));
-      const int grow = (isw ? w0 : t0) + row;
-      off[i] = (grow < (isw ? Nw : Tv)) ? grow * K + c * 8 : -1;
+      const int grow = min((isw ? w0 : t0) + row, (isw ? Nw : Tv) - 1);
+      gsrc[i] = (isw ? W : X) + (size_t)grow * K + c * 8;
       kc[i] = c * 8;
     }
     const bool ktail = (K % KD) != 0;
+    const uint32_t lds0 = lds_addr_of(sm) + (uint32_t)(__builtin_amdgcn_readfirstlane(wid) * IPW) * 1024u;
     auto issue = [&](int kt) {
-      const uint4* stage = sm + (kt % STAGES) * CH;
+      const uint32_t stage = lds0 + (uint32_t)((kt % STAGES) * CH) * 16u;
       const int k0 = (kb + kt) * KD;
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
-        const int q = wid * IPW + i;
-        const bf16_t* base = (q * 64 < BW * CPR) ? W : X;
-        const bool ok = off[i] >= 0 && (!ktail || k0 + kc[i] < K);
-        dma16(ok ? static_cast<const void*>(base + (size_t)off[i] + k0) : static_cast<const void*>(g_zero_chunk),
-              stage + q * 64);
+        const bf16_t* g = gsrc[i] + k0;
+        if (ktail && k0 + kc[i] >= K) g = reinterpret_cast<const bf16_t*>(g_zero_chunk);
+        dma16_lds(g, stage + (uint32_t)i * 1024u);
       }
     };
     auto frag = [&](int kt, int ks, bf16x8_t(&a)[SW], bf16x8_t(&b)[ST]) {
@@ -436,6 +442,13 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
         for (int j = 0; j < ST; ++j) acc[i][j] = mfma16(a[i], b[j], acc[i][j]);
     };
 
+    auto mma_rows = [&](const bf16x8_t(&a)[SW], const bf16x8_t(&b)[ST], int i0, int i1) {
+#pragma unroll
+      for (int i = 0; i < SW; ++i)
+        if (i >= i0 && i < i1)
+#pragma unroll
+          for (int j = 0; j < ST; ++j) acc[i][j] = mfma16(a[i], b[j], acc[i][j]);
+    };
 #pragma unroll
     for (int st = 0; st < STAGES; ++st)
       if (st < nk) issue(st);
@@ -461,8 +474,19 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
           else if (STAGES >= 3 && pend >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * IPW>();
           else wait_vmcnt<0>();
           lds_barrier();
-          if (kt + STAGES < nk) issue(kt + STAGES);
-          frag(kt + 1, 0, fa[0], fb[0]);
+          if constexpr (STAGES >= 3) {
+            // the next stage's first fragments go out first, and the refill is issued between two
+            // halves of this substep's MFMAs, so its address work overlaps the matrix pipe
+            frag(kt + 1, 0, fa[0], fb[0]);
+            mma_rows(fa[s & 1], fb[s & 1], 0, (SW + 1) / 2);
+            if (kt + STAGES < nk) issue(kt + STAGES);
+            mma_rows(fa[s & 1], fb[s & 1], (SW + 1) / 2, SW);
+            continue;
+          } else {
+            // one stage in flight: the refill goes out at once, ahead of everything else
+            if (kt + STAGES < nk) issue(kt + STAGES);
+            frag(kt + 1, 0, fa[0], fb[0]);
+          }
         }
         mma(fa[s & 1], fb[s & 1]);
       }
