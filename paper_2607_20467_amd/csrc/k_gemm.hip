@@ -352,7 +352,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi>
+template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi, bool KTAIL>
 __global__ void __launch_bounds__(WW * WT * 64)
 gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, int T, int K,
             const int32_t* __restrict__ t_count, int nsplit, Epi epi) {
@@ -389,8 +389,8 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
 
     // Per-lane source of this wave's load instructions at K offset 0. A row outside the operand
     // is clamped to the last valid row: its data only reaches accumulators of rows / tokens that
-    // every epilogue skips, so no zero fill is needed. Without a K tail the source of stage kt is
-    // this pointer plus (kb + kt) * KD elements; with one, chunks past K read the zero chunk.
+    // every epilogue skips, so no zero fill is needed. The source of stage kt is this pointer plus
+    // (kb + kt) * KD elements; with KTAIL (K not a multiple of KD), chunks past K read the zero chunk.
     const bf16_t* gsrc[IPW];
     int kc[IPW];
 #pragma unroll
@@ -404,7 +404,6 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
       gsrc[i] = (isw ? W : X) + (size_t)grow * K + c * 8;
       kc[i] = c * 8;
     }
-    const bool ktail = (K % KD) != 0;
     const uint32_t lds0 = lds_addr_of(sm) + (uint32_t)(__builtin_amdgcn_readfirstlane(wid) * IPW) * 1024u;
     auto issue = [&](int kt) {
       const uint32_t stage = lds0 + (uint32_t)((kt % STAGES) * CH) * 16u;
@@ -412,7 +411,8 @@ gemm_kernel(const bf16_t* __restrict__ W, const bf16_t* __restrict__ X, int Nw, 
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
         const bf16_t* g = gsrc[i] + k0;
-        if (ktail && k0 + kc[i] >= K) g = reinterpret_cast<const bf16_t*>(g_zero_chunk);
+        if constexpr (KTAIL)
+          if (k0 + kc[i] >= K) g = reinterpret_cast<const bf16_t*>(g_zero_chunk);
         dma16_lds(g, stage + (uint32_t)i * 1024u);
       }
     };
@@ -735,7 +735,7 @@ void gemm_cfg_shape(int cfg, int* shape) {
   shape[5] = c.wt;
 }
 
-template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi>
+template <int BW, int BT, int KD, int STAGES, int WW, int WT, class Epi, bool KTAIL = false>
 static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count, int nsplit,
                     const Epi& epi, hipStream_t s) {
   const int tiles = ((Nw + BW - 1) / BW) * ((T + BT - 1) / BT);
@@ -746,7 +746,7 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
   int grid = 8 * ((units + 7) / 8);
   if (t_count && grid > 8 * kCUs) grid = 8 * kCUs;
   const size_t lds = (size_t)STAGES * (BW + BT) * (KD / 8) * 16;
-  auto kern = gemm_kernel<BW, BT, KD, STAGES, WW, WT, Epi>;
+  auto kern = gemm_kernel<BW, BT, KD, STAGES, WW, WT, Epi, KTAIL>;
   // per instantiation: the ring plus the epilogue's static LDS fit in a CU (-1 = not yet known)
   static std::atomic<int> fits{-1};
   if (fits.load(std::memory_order_acquire) < 0) {
@@ -756,7 +756,7 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
                std::memory_order_release);
   }
   if (!fits.load(std::memory_order_acquire)) {  // never planned (plans respect kLdsBytes); keep a launch the
-    run_cfg<128, 128, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, nsplit, epi, s);  // runtime would reject off the GPU
+    run_cfg<128, 128, 64, 2, 2, 4, Epi, KTAIL>(W, X, Nw, T, K, t_count, nsplit, epi, s);  // runtime would reject off the GPU
     return;
   }
   static std::atomic<uint32_t> lds_set{0};
@@ -770,6 +770,12 @@ template <class Epi>
 static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
                      const Epi& epi, hipStream_t s) {
   const int n = p.nsplit;
+  if (!kCfgs[p.cfg].rp && K % kCfgs[p.cfg].kd != 0) {
+    // K is not a multiple of the plan's stage depth: one tail-aware configuration serves every such
+    // shape (none of the tuned model shapes), so the tuned kernels carry no tail handling
+    run_cfg<128, 128, 64, 2, 2, 4, Epi, true>(W, X, Nw, T, K, t_count, n, epi, s);
+    return;
+  }
   switch (p.cfg) {
     case 0: run_cfg<128, 128, 64, 2, 2, 4>(W, X, Nw, T, K, t_count, n, epi, s); break;
     case 1: run_cfg<192, 192, 64, 3, 4, 2>(W, X, Nw, T, K, t_count, n, epi, s); break;
