@@ -755,9 +755,15 @@ static void run_cfg(const bf16_t* W, const bf16_t* X, int Nw, int T, int K, cons
                    at.sharedSizeBytes + lds <= kLdsBytes,
                std::memory_order_release);
   }
-  if (!fits.load(std::memory_order_acquire)) {  // never planned (plans respect kLdsBytes); keep a launch the
-    run_cfg<128, 128, 64, 2, 2, 4, Epi, KTAIL>(W, X, Nw, T, K, t_count, nsplit, epi, s);  // runtime would reject off the GPU
-    return;
+  // A ring that does not fit is never planned (plans respect kLdsBytes). Rather than a launch the runtime
+  // would reject, the smallest configuration runs; that one always fits and is launched even if the
+  // attribute query itself failed, so this never recurses.
+  constexpr bool kSmallest = BW == 128 && BT == 128 && KD == 64 && STAGES == 2 && WW == 2 && WT == 4;
+  if constexpr (!kSmallest) {
+    if (!fits.load(std::memory_order_acquire)) {
+      run_cfg<128, 128, 64, 2, 2, 4, Epi, KTAIL>(W, X, Nw, T, K, t_count, nsplit, epi, s);
+      return;
+    }
   }
   static std::atomic<uint32_t> lds_set{0};
   ensure_dynamic_lds(reinterpret_cast<const void*>(kern), lds, lds_set);
