@@ -15,7 +15,6 @@ pytestmark = pytest.mark.gpu
 
 
 def test_noalloc_step_matches_workspace_step():
-    import torch
     import paper_2607_20467_amd as dcl
     base = synth.WORKLOADS["c1s"]
     small = dataclasses.replace(base, batch=1, prompt_len=20, gen_len=44, window=16, p=20, draft=(36, 44))
