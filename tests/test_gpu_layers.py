@@ -52,9 +52,10 @@ def _layer_weights(view, geom, l):
 class _Case:
     """GPU-side state of one workload: decode state, cache, the residual stream and the tap buffers."""
 
-    def __init__(self, key, run, stored):
+    def __init__(self, w, run, stored):
         import torch
-        self.key, self.w, self.run = key, synth.WORKLOADS[key], run
+        w = synth.WORKLOADS[w] if isinstance(w, str) else w
+        self.key, self.w, self.run = w.key, w, run
         w, g = self.w, self.w.geom
         self.tok, self.p = synth.initial_state(w)
         self.B, self.S = self.tok.shape
@@ -64,8 +65,15 @@ class _Case:
         self.kv = None
         if self.P:
             self.kv_host = [synth.kv_cache_layer(w, l) for l in range(g.n_layers)]
-            self.kv = ([torch.from_numpy(c[0].view(np.int16)).cuda() for c in self.kv_host],
-                       [torch.from_numpy(c[1].view(np.int16)).cuda() for c in self.kv_host], self.P)
+            cap = (self.P + 7) // 8 * 8       # cache capacity: positions [0, P) in use
+
+            def pad(x, axis):
+                shape = list(x.shape)
+                shape[axis] = cap
+                out = np.zeros(shape, x.dtype)
+                out[(slice(None),) * axis + (slice(0, self.P),)] = x
+                return torch.from_numpy(out.view(np.int16)).cuda()
+            self.kv = ([pad(c[0], 2) for c in self.kv_host], [pad(c[1], 3) for c in self.kv_host], self.P, cap)
         self.t_dev, self.p_dev = to_dev(self.tok), to_dev(self.p)
         emb = synth.bf16_bits_to_f32(stored["embed"][self.tok])          # r_0 = E[x] widened exactly
         self.r = torch.from_numpy(emb.reshape(self.T, g.d_model)).cuda()
@@ -220,10 +228,11 @@ def _final_and_head(case, view):
     return rep
 
 
-def _run_geometry(keys):
-    w0 = synth.WORKLOADS[keys[0]]
+def _run_geometry(keys, stored=None, run=None):
+    w0 = synth.WORKLOADS[keys[0]] if isinstance(keys[0], str) else keys[0]
     g = w0.geom
-    stored, run = full_runner(w0)
+    if run is None:
+        stored, run = full_runner(w0)
     view = WeightView(stored)
     cases = [_Case(k, run, stored) for k in keys]
     flips = {}
@@ -259,6 +268,24 @@ def test_every_layer_stagewise_llada8b():
     """c2 (B1 x 384), c3 (B1 x 1280) and c5 (B8 x 64 after a 1216-key cached prefix): LLaDA-8B
     geometry, all 32 layers."""
     _run_geometry(["c2", "c3", "c5"])
+
+
+# Ragged shapes at the same bounds: d_model 208 and d_ffn 400 are not multiples of the 64-deep stages
+# (every GEMM runs its K-tail variant), 3 x 37 tokens, 13 / 208 / 800 / 256 weight rows and a 1000-id
+# vocabulary do not fill their tiles (rows outside an operand are clamped), H * dh = 256 != d_model,
+# GQA 4/2 with q/k/v biases, and a 13-token cached prefix (5 carried keys in front of the fresh ones).
+_ODD = synth.Workload("odd_shapes", dataclasses.replace(synth.WORKLOADS["c1s"].geom, name="odd-shapes", n_layers=2,
+                                                        n_heads=4, n_kv_heads=2, head_dim=64, d_model=208, d_ffn=400,
+                                                        vocab=1000, mask_id=999, qkv_bias=True, weight_dtype="bf16",
+                                                        rope_base=1e6),
+                      batch=3, prompt_len=0, gen_len=37, window=16, p=0, draft=(20, 37), tau_commit=0.7,
+                      tau_draft=0.98, kv_prefix=13, kv_seed=5)
+
+
+def test_every_layer_stagewise_ragged_shapes():
+    """Both layers of a small GQA + bias geometry whose every dimension leaves partial tiles and K tails."""
+    stored = synth.make_weights(_ODD.geom)
+    _run_geometry([_ODD], stored, runner_for(_ODD, stored))
 
 
 # ---------------------------------------------------------------- LM head on its production plans
