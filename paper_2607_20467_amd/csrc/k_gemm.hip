@@ -720,6 +720,10 @@ GemmPlan plan_gemm(int Nw, int T, int K, int force_bw, int max_split) {
       }
     }
   }
+  // K not a multiple of the plan's stage depth: one tail-aware configuration (128 x 128, 64-deep stages,
+  // which also suits the LM head's split layout) serves every such shape, none of the tuned model
+  // shapes, so the tuned kernels carry no tail handling; the register-prefetch kernel handles tails itself
+  if (!kCfgs[best.cfg].rp && K % kCfgs[best.cfg].kd != 0) best.cfg = 0;
   const TileCfg& c = kCfgs[best.cfg];
   best.tiles = ((Nw + c.bw - 1) / c.bw) * ((T + c.bt - 1) / c.bt);
   return best;
@@ -776,9 +780,7 @@ template <class Epi>
 static void run_plan(const GemmPlan& p, const bf16_t* W, const bf16_t* X, int Nw, int T, int K, const int32_t* t_count,
                      const Epi& epi, hipStream_t s) {
   const int n = p.nsplit;
-  if (!kCfgs[p.cfg].rp && K % kCfgs[p.cfg].kd != 0) {
-    // K is not a multiple of the plan's stage depth: one tail-aware configuration serves every such
-    // shape (none of the tuned model shapes), so the tuned kernels carry no tail handling
+  if (!kCfgs[p.cfg].rp && K % kCfgs[p.cfg].kd != 0) {  // plan_gemm gives such shapes configuration 0
     run_cfg<128, 128, 64, 2, 2, 4, Epi, true>(W, X, Nw, T, K, t_count, n, epi, s);
     return;
   }

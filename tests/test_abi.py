@@ -194,3 +194,16 @@ def test_noalloc_step_rejects_sizes_beyond_its_scratch_on_the_host(dcl):
         assert r == 5 and "not loaded" in dcl.dcl_last_error()
     finally:
         dcl.dcl_model_destroy(m)
+
+
+@pytest.mark.parametrize("nw,t,k,lm", [(24576, 384, 4096, False), (4096, 384, 12288, False), (126464, 384, 4096, True),
+                                       (800, 111, 208, False), (208, 111, 400, False), (1000, 60, 208, True),
+                                       (4608, 3072, 3584, False), (12288, 1280, 4160, False)])
+def test_gemm_plans_fit_their_depth(dcl, nw, t, k, lm):
+    """The reported plan is the one that runs: its stage depth divides K (the tuned kernels carry no K-tail
+    handling), except for the single tail-aware configuration 0 that serves every other K; an LM-head plan
+    is one of the two vocabulary-tile layouts the fused epilogue is written for."""
+    plan = dcl.dcl_debug_gemm_plan(nw, t, k, lm_head=lm)
+    assert k % plan["kd"] == 0 or plan["cfg"] == 0, plan
+    if lm:
+        assert plan["bw"] // plan["ww"] == 128 or (plan["bw"] == 128 and plan["ww"] == 2), plan
