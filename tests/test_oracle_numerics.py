@@ -34,6 +34,19 @@ def test_bf16_round_ties_to_even():
     assert bf16_round(np.array([-(1.0 + 2.0 ** -8 + 2.0 ** -40)]))[0] == -(1.0 + 2.0 ** -7)
 
 
+def test_weight_values_widen_bf16_bits_exactly():
+    """Stored weights: bf16 bit patterns widen exactly (as torch's bfloat16 -> float64), float arrays round
+    to bf16 in bf16-boundary mode and stay as they are in pure mode."""
+    from oracle.numerics import weight_values
+    rng = np.random.default_rng(11)
+    x = (rng.standard_normal(5000) * 0.05).astype(np.float32)
+    bits = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(weight_values(bits), ref)
+    np.testing.assert_array_equal(weight_values(x.astype(np.float64)), ref)
+    np.testing.assert_array_equal(weight_values(x, bf16_boundary=False), x.astype(np.float64))
+
+
 def test_rmsnorm_matches_torch():
     rng = np.random.default_rng(1)
     r = rng.standard_normal((7, 96)) * 3
