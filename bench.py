@@ -248,7 +248,7 @@ def main():
         print(json.dumps({"source_digest": kernel_source_digest(), "classes": summ}, indent=1))
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
+        print(f"bench.py measures one GPU: the library has no multi-GPU path (asked for --gpus {args.gpus}); "
               "one process drives one GPU", file=sys.stderr)
         sys.exit(2)
 

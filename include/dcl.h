@@ -42,7 +42,7 @@ extern "C" {
 typedef enum {
   DCL_OK = 0,
   DCL_E_ARG = 1,          /* null pointer, size or range outside the documented domain */
-  DCL_E_UNSUPPORTED = 2,  /* geometry this build has no kernels for */
+  DCL_E_UNSUPPORTED = 2,  /* geometry the library has no kernels for */
   DCL_E_WORKSPACE = 3,    /* workspace or weight buffer smaller than required */
   DCL_E_HIP = 4,          /* a HIP runtime call or kernel launch failed */
   DCL_E_STATE = 5         /* object used in the wrong state (e.g. step before weights load) */
