@@ -149,7 +149,9 @@ struct AttnArgs {
   bf16_t* o;                     // [B,S,H*dh]
   int B, H, Hkv, dh, S, Sp, P, Pc;
   float scale_log2;              // log2(e) / sqrt(dh)
-  int Sk = 0;                    // fresh keys per (b, kv head); 0: Sk = S. P must be a multiple of 8.
+  int Sk = 0;                    // keys per (b, kv head) in k / vt; 0: Sk = S. P (the keys read from the
+                                 // cache) must be a multiple of 8: the P mod 8 newest cached keys of a
+                                 // ragged prefix are carried into the front of k / vt (Sk = P mod 8 + S)
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
 // The koff = P mod 8 newest cached keys [P - koff, P) and their values into slots [0, koff) of the fresh
