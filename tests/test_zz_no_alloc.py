@@ -1,7 +1,9 @@
 """dcl_denoise_step_noalloc (the step with its workspace in the library's static scratch, for callers
 that cannot allocate) against dcl_denoise_step with a caller workspace: the same kernels on the same
 inputs, so the statistics must be identical bit for bit. Two calls in a row, the second on a smaller
-input, check that the shared scratch carries nothing from one call into the next."""
+input, check that the shared scratch carries nothing from one call into the next. The refusal of a step
+whose workspace exceeds the scratch is a host-side check, tested without a GPU in test_abi.py (no GPU
+test hands the library addresses that only that check keeps from being used)."""
 import dataclasses
 
 import numpy as np
@@ -35,15 +37,3 @@ def test_noalloc_step_matches_workspace_step():
             np.testing.assert_array_equal(got[k], ref[k], err_msg=f"{k} differs at B={B} S={S}")
         assert (ref["conf"] >= 0).sum() > 0
 
-
-def test_noalloc_rejects_steps_beyond_the_scratch():
-    import paper_2607_20467_amd as dcl
-    w = synth.WORKLOADS["c1s"]
-    run = runner_for(w, synth.make_weights(w.geom))
-    need = dcl.dcl_workspace_bytes(run.model, 1, 4096, 0)
-    B = dcl.DCL_NOALLOC_SCRATCH_BYTES // need + 1
-    lib = dcl.load_library()
-    st = dcl.binding.DclRowStats(256, 256, 256, 256, 256)
-    # rejected on the host before any launch (the pointers are never dereferenced)
-    assert lib.dcl_denoise_step_noalloc(run.model, 256, B, 4096, 256, 4096, None, 0, st, None) == 3
-    assert "static scratch" in dcl.dcl_last_error()
